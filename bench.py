@@ -1,0 +1,202 @@
+#!/usr/bin/env python3
+"""Throughput of the MXFP4 attention forward (quantize Q/K/V + fused kernel)
+on one MI355X, on synthetic video-DiT-shaped inputs.
+
+    python bench.py [--steps K] [--warmup W] [--workload video720p] [--mode uos_pnq]
+
+Prints one JSON line.  ``value`` is 4*B*H*N^2*d / t in TFLOP/s for the whole
+forward (the three quantize launches and the fused attention kernel), inputs
+already resident in HBM.  ``roofline`` rates the fused attention kernel alone
+against the dense MXFP4 matrix-core peak; ``cpu_baseline`` times the CPU
+oracle on a bounded sample of the same workload on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "MXFP4 attn fwd TFLOPS (4·B·H·N²·d/t) & % of MXFP4 MFMA peak, N=75600"
+PEAK_FP4_TFLOPS = 10100.0  # MI355X dense MXFP4 matrix-core peak, 10.1 PFLOP/s
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attention_video720p_hbm_traffic.json")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_24377_amd", "csrc", "attention.hip")
+
+
+def log(msg: str):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def time_ms(fn, steps: int, warmup: int, torch) -> float:
+    """Average ms per call over `steps` calls after `warmup` calls, bracketed by
+    device synchronizations, timed with events on the current stream."""
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        fn()
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / steps
+
+
+def measured_traffic():
+    """HBM bytes per launch of the attention kernel from the committed PMC
+    counter summary, if it was taken on the current kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+        with open(KERNEL_SOURCE, "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()
+        if rec.get("kernel_source_sha256") != sha:
+            return None
+        return float(rec["hbm_bytes_per_launch"])
+    except (OSError, ValueError, KeyError):
+        return None
+
+
+def cpu_baseline(w, mode: str, rows_req: int, q_bits, k_bits, v_bits):
+    """Time the CPU oracle on sampled query rows of head 0 (its own quantization
+    of that head, then the tiled recurrence over all N keys)."""
+    import numpy as np
+
+    import oracle
+
+    qh, kh, vh = (x.reshape((-1,) + x.shape[2:])[0:1][None] for x in (q_bits, k_bits, v_bits))
+    codes = oracle.quantize_qkv(qh, kh, vh, mode)
+
+    def run(rows):
+        return oracle.mx_attention_head_rows(codes["qc"][0, 0], codes["qs"][0, 0], codes["kc"][0, 0],
+                                             codes["ks"][0, 0], codes["vc"][0, 0], codes["vs"][0, 0],
+                                             w.N, rows, mode, 128)
+
+    nthreads = oracle.threads(0)
+    rng = np.random.default_rng(1)
+    if rows_req <= 0:  # size the sample for ~15 s of CPU work
+        probe = rng.choice(w.N, size=min(w.N, nthreads), replace=False)
+        t0 = time.perf_counter()
+        run(probe)
+        dt = time.perf_counter() - t0
+        rows_req = int(max(nthreads, min(8192, 15.0 / max(dt, 1e-6) * probe.size)))
+    rows = np.sort(rng.choice(w.N, size=min(w.N, rows_req), replace=False))
+    t0 = time.perf_counter()
+    run(rows)
+    dt = time.perf_counter() - t0
+    flops = 4.0 * w.N * w.d * rows.size
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": nthreads, "kind": "oracle",
+            "sample": f"{rows.size} random query rows of head 0 of {w.name} ({mode}), all "
+                      f"{w.N} keys, fp64 tiled recurrence incl. dequantization; "
+                      f"{dt:.1f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="video720p")
+    ap.add_argument("--mode", default="uos_pnq", choices=["ocp_vanilla", "uos", "uos_pnq"])
+    ap.add_argument("--cpu-rows", type=int, default=0, help="oracle sample rows (0: ~15 s)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-overhead", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+              "the path shards over heads without communication, see the design notes.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2607_24377_amd import inputs, mxattn
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = inputs.workload(args.workload)
+    log(f"[bench] generating {w.name} B={w.B} H={w.H} N={w.N} d={w.d}")
+    q_bits, k_bits, v_bits = inputs.generate(w)
+    q, k, v = (mxattn.bf16_from_bits(x, dev) for x in (q_bits, k_bits, v_bits))
+    out = torch.empty_like(q)
+    mxattn.lib()
+
+    def fwd(mode):
+        return lambda: mxattn.forward(q, k, v, mode, out=out)
+
+    log(f"[bench] timing forward {args.mode}: warmup {args.warmup}, steps {args.steps}")
+    ms = time_ms(fwd(args.mode), args.steps, args.warmup, torch)
+    value = w.flops / (ms * 1e-3) / 1e12
+
+    # the fused attention kernel alone (dominant kernel) on pre-quantized operands
+    qc, qs = mxattn.quantize(q, mxattn.AXIS_HEAD_DIM, args.mode)
+    kc, ks = mxattn.quantize(k, mxattn.AXIS_HEAD_DIM, args.mode)
+    vc, vs = mxattn.quantize(v, mxattn.AXIS_TOKENS, args.mode)
+    log("[bench] timing the attention kernel alone")
+    attn_ms = time_ms(lambda: mxattn.attend(qc, qs, kc, ks, vc, vs, w.N, args.mode, out=out),
+                      args.steps, 1, torch)
+    quant_ms = time_ms(lambda: mxattn.quantize(v, mxattn.AXIS_TOKENS, args.mode, codes=vc, scales=vs),
+                       args.steps, 1, torch)
+    quant_q_ms = time_ms(lambda: mxattn.quantize(q, mxattn.AXIS_HEAD_DIM, args.mode, codes=qc, scales=qs),
+                         args.steps, 1, torch)
+    achieved = w.flops / (attn_ms * 1e-3) / 1e12
+    elems = w.B * w.H * w.N * w.d
+    extra = {
+        "pct_of_mxfp4_peak": 100.0 * value / PEAK_FP4_TFLOPS,
+        "attention_kernel_ms": attn_ms,
+        "quantize_headdim_ms": quant_q_ms,
+        "quantize_tokens_ms": quant_ms,
+        "quantize_headdim_GBps": elems * 2.53125 / (quant_q_ms * 1e-3) / 1e9,
+        "quantize_tokens_GBps": elems * 2.53125 / (quant_ms * 1e-3) / 1e9,
+    }
+    if not args.no_overhead:
+        other = "ocp_vanilla" if args.mode != "ocp_vanilla" else "uos_pnq"
+        log(f"[bench] timing forward {other} for the overhead comparison")
+        ms_other = time_ms(fwd(other), args.steps, 1, torch)
+        ms_again = time_ms(fwd(args.mode), args.steps, 1, torch)
+        extra[f"{other}_ms_per_step"] = ms_other
+        extra[f"{args.mode}_ms_per_step_repeat"] = ms_again
+        extra[f"overhead_{args.mode}_vs_{other}"] = min(ms, ms_again) / ms_other - 1.0
+    del qc, qs, kc, ks, vc, vs
+
+    result = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "mxfp4",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "N": w.N, "d": w.d, "mode": args.mode,
+                   "kv_tile": mxattn.kv_tile(), "query_tile": mxattn.query_tile()},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP4_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_FP4_TFLOPS,
+                     "traffic": measured_traffic()},
+    }
+    result.update(extra)
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle baseline")
+        result["cpu_baseline"] = cpu_baseline(w, args.mode, args.cpu_rows, q_bits, k_bits, v_bits)
+    else:
+        result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,144 @@
+/*
+ * mxattn.h -- C ABI of libmxattn: MXFP4 attention forward for MI355X (gfx950).
+ *
+ * The library implements the hot path of "MXAttention: Data-Free Optimal
+ * Scaling and Pre-Normalization Quantization for MXFP4 Attention":
+ *
+ *   1. an MXFP4 quantizer (32-element E2M1 blocks sharing one E8M0
+ *      power-of-two scale) with either the OCP floor scale rule
+ *      e = floor(log2 M) - 2 (Sec. 2, Eq. ocp_scale) or the Universal Optimal
+ *      Scaling rule e = ceil(log2(M / 7.25)) (Sec. 4.1, Algorithm 1);
+ *   2. a fused flash-style attention forward on MXFP4 Q, K, V: S = Q^K^T on
+ *      block-scaled FP4 matrix cores, online softmax, in-register MXFP4
+ *      quantization of the unnormalized exponential tile, and O~ += P^V^ on
+ *      FP4 matrix cores (Algorithm 2 without its Hadamard rotation).
+ *
+ * Everything is asynchronous on the caller's HIP stream.  All tensor
+ * pointers are device pointers owned by the caller; the library never frees
+ * or retains them.  Arguments are validated before anything is launched; on
+ * an error nothing is launched and a nonzero status is returned.  The library
+ * never aborts, prints or throws.  Inputs must be finite (not checked).
+ *
+ * Layouts (row-major, bf16 = IEEE binary32 truncated to its top 16 bits):
+ *   Q, K, V, O        bf16 [B, H, N, d], d = 128.
+ *   head-dim blocks   (block_axis = 3, used for Q and K): 32 consecutive
+ *                     channels of one token.
+ *                     codes  uint8 [B, H, N, d/2]   element 2i in the low
+ *                                                   nibble of byte i
+ *                     scales uint8 [B, H, N, d/32]  E8M0 (bias 127)
+ *   token blocks      (block_axis = 2, used for V): 32 consecutive tokens of
+ *                     one channel; the last block of a row is padded with +0.
+ *                     codes  uint8 [B, H, d, nb*16] nb = ceil(N/32), tokens
+ *                                                   contiguous per channel
+ *                     scales uint8 [B, H, d, nb]
+ *   A 4-bit code is sign(1) | magnitude index(3) into the E2M1 grid
+ *   {0, 0.5, 1, 1.5, 2, 3, 4, 6} (Sec. 2, "MXFP4 Block Quantization").
+ *
+ * Rounding of the quantizer (readings of the paper, which says only "round
+ * to nearest with saturation at +-6"): ties go to the even code, magnitudes
+ * above 6 saturate to 6, the code keeps the input's sign bit even for a zero
+ * magnitude, the E8M0 exponent is clamped to [-127, 127], and an all-zero
+ * block gets scale byte 127 (sigma = 1, as Algorithm 1 states).
+ */
+#ifndef MXATTN_H
+#define MXATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Scale rule and row-sum placement (the rows of the paper's sequential
+ * ablation, Sec. 5.3, without the Hadamard rotation):
+ *   MXATTN_OCP_VANILLA  OCP floor rule for Q, K, V and P~; direct placement:
+ *                       l accumulates the unquantized P~ (Eq.
+ *                       direct_mxfp4_tile, Sec. 4.2).
+ *   MXATTN_UOS          UOS rule (Algorithm 1) everywhere; direct placement.
+ *   MXATTN_UOS_PNQ      UOS rule everywhere; Pre-Normalization Quantization:
+ *                       l accumulates the quantized P^ that also feeds the PV
+ *                       product (Eqs. pnq_tile_contribution and
+ *                       pnq_online_update; Algorithm 2). */
+typedef enum {
+    MXATTN_OCP_VANILLA = 0,
+    MXATTN_UOS = 1,
+    MXATTN_UOS_PNQ = 2
+} mxattn_mode;
+
+typedef enum {
+    MXATTN_OK = 0,
+    MXATTN_ERR_NULL = 1,        /* a required pointer is NULL              */
+    MXATTN_ERR_SHAPE = 2,       /* B, H or N < 1, or a size overflows       */
+    MXATTN_ERR_ALIGN = 3,       /* a pointer is not 16-byte aligned         */
+    MXATTN_ERR_MODE = 4,        /* mode is not an mxattn_mode value         */
+    MXATTN_ERR_AXIS = 5,        /* block_axis is not 2 or 3                 */
+    MXATTN_ERR_UNSUPPORTED = 6, /* d != 128                                 */
+    MXATTN_ERR_OOM = 7,         /* workspace allocation failed              */
+    MXATTN_ERR_HIP = 8          /* a HIP call failed; see mxattn_last_error */
+} mxattn_status;
+
+#define MXATTN_AXIS_TOKENS 2   /* blocks along N (V)      */
+#define MXATTN_AXIS_HEAD_DIM 3 /* blocks along d (Q and K) */
+
+/* MXFP4-quantize a bf16 tensor x [B, H, N, d] (Algorithm 1 with the scale
+ * rule of `mode`: OCP floor for MXATTN_OCP_VANILLA, UOS otherwise).
+ *   x       device, bf16 [B, H, N, d], 16-byte aligned
+ *   codes   device, layout of `block_axis` above, 16-byte aligned,
+ *           mxattn_codes_bytes() bytes
+ *   scales  device, layout of `block_axis` above, mxattn_scales_bytes() bytes
+ *   stream  hipStream_t to run on (NULL: the null stream)
+ * Returns MXATTN_OK or an error status; nothing is launched on error. */
+int mxattn_quantize(const void* x, uint8_t* codes, uint8_t* scales, int block_axis, int mode,
+                    int64_t B, int64_t H, int64_t N, int64_t d, void* stream);
+
+/* MXFP4 attention forward O = softmax(Q K^T / sqrt(d)) V with MXFP4 Q, K, V
+ * and MXFP4 P~ (Algorithm 2 without rotation; non-causal, no mask besides
+ * the sequence end).  Quantizes Q and K along d and V along N into
+ * stream-ordered workspace (hipMallocAsync/hipFreeAsync on `stream`, about
+ * 0.53 bytes per element of each of Q, K, V), then runs the fused kernel.
+ *   q, k, v  device bf16 [B, H, N, d], 16-byte aligned
+ *   out      device bf16 [B, H, N, d], 16-byte aligned, must not alias inputs
+ * Returns MXATTN_OK, MXATTN_ERR_OOM if the workspace cannot be allocated, or
+ * another error status. */
+int mxattn_forward(const void* q, const void* k, const void* v, void* out, int64_t B, int64_t H,
+                   int64_t N, int64_t d, int mode, void* stream);
+
+/* The fused attention kernel alone, on already quantized operands (the
+ * layouts above: Q and K blocked along d, V blocked along N).  The scale rule
+ * of `mode` applies to the in-kernel quantization of P~; `mode` also selects
+ * direct or PNQ placement.  All pointers are device pointers; code arrays
+ * and `out` are 16-byte aligned, k_scales 4-byte aligned, the other scale
+ * arrays may have any alignment. */
+int mxattn_attend(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
+                  const uint8_t* k_scales, const uint8_t* v_codes, const uint8_t* v_scales,
+                  void* out, int64_t B, int64_t H, int64_t N, int64_t d, int mode, void* stream);
+
+/* Sizes of the code and scale arrays of a [B, H, N, d] tensor blocked along
+ * `block_axis`; 0 for invalid arguments. */
+size_t mxattn_codes_bytes(int block_axis, int64_t B, int64_t H, int64_t N, int64_t d);
+size_t mxattn_scales_bytes(int block_axis, int64_t B, int64_t H, int64_t N, int64_t d);
+
+/* KV tile width B_c of the fused kernel: the running maximum is updated once
+ * per B_c keys, in increasing key order (this fixes which exponentials are
+ * quantized together; see Sec. 2, Eq. online_attention). */
+int mxattn_kv_tile(void);
+
+/* Query rows handled by one workgroup of the fused kernel. */
+int mxattn_query_tile(void);
+
+/* Static description of a status code. */
+const char* mxattn_status_string(int status);
+
+/* Detail of the last MXATTN_ERR_HIP or MXATTN_ERR_OOM on the calling
+ * thread ("" if none). */
+const char* mxattn_last_error(void);
+
+/* ABI version (major * 100 + minor). */
+int mxattn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MXATTN_H */

@@ -1,0 +1,211 @@
+// api.hip -- the extern "C" entry points of libmxattn (see include/mxattn.h).
+//
+// Argument validation happens before any HIP call, so every error path is
+// free of device work.  The only global state is a once-per-device setting
+// of the stream-ordered allocator's release threshold (so the forward's
+// workspace is recycled by the pool instead of being returned to the driver
+// at every synchronization).
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+
+#include "../../include/mxattn.h"
+#include "launch.h"
+
+namespace {
+
+thread_local char g_last_error[256] = "";
+
+void set_error(const char* what, hipError_t e) {
+    std::snprintf(g_last_error, sizeof g_last_error, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+bool valid_mode(int mode) { return mode >= MXATTN_OCP_VANILLA && mode <= MXATTN_UOS_PNQ; }
+
+// Shape limits of the kernels: 32-bit token indices, 64-bit byte offsets.
+int check_shape(int64_t B, int64_t H, int64_t N, int64_t d) {
+    if (B < 1 || H < 1 || N < 1 || d < 1) return MXATTN_ERR_SHAPE;
+    if (B > (1 << 20) || H > (1 << 20) || N > (1 << 28)) return MXATTN_ERR_SHAPE;
+    if (B * H > (int64_t)1 << 24) return MXATTN_ERR_SHAPE;
+    if (d != 128) return MXATTN_ERR_UNSUPPORTED;
+    return MXATTN_OK;
+}
+
+int rule_of(int mode) { return mode == MXATTN_OCP_VANILLA ? mxattn::kRuleOcp : mxattn::kRuleUos; }
+
+constexpr int kMaxDevices = 64;
+std::once_flag g_pool_once[kMaxDevices];
+
+void keep_pool_memory() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return;
+    std::call_once(g_pool_once[dev], [dev] {
+        hipMemPool_t pool;
+        if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
+            uint64_t threshold = UINT64_MAX;
+            (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &threshold);
+        }
+    });
+}
+
+}  // namespace
+
+extern "C" {
+
+int mxattn_version(void) { return 100; }
+
+int mxattn_kv_tile(void) { return mxattn::kKvTile; }
+
+int mxattn_query_tile(void) { return mxattn::kQueryTile; }
+
+const char* mxattn_status_string(int s) {
+    switch (s) {
+        case MXATTN_OK: return "ok";
+        case MXATTN_ERR_NULL: return "null pointer argument";
+        case MXATTN_ERR_SHAPE: return "invalid shape (B, H, N must be >= 1 and within limits)";
+        case MXATTN_ERR_ALIGN: return "misaligned pointer (tensors need 16-byte alignment)";
+        case MXATTN_ERR_MODE: return "invalid mode (0 ocp_vanilla, 1 uos, 2 uos_pnq)";
+        case MXATTN_ERR_AXIS: return "invalid block_axis (2 = tokens, 3 = head dim)";
+        case MXATTN_ERR_UNSUPPORTED: return "unsupported head dimension (d must be 128)";
+        case MXATTN_ERR_OOM: return "workspace allocation failed";
+        case MXATTN_ERR_HIP: return "HIP runtime error";
+        default: return "unknown status";
+    }
+}
+
+const char* mxattn_last_error(void) { return g_last_error; }
+
+size_t mxattn_codes_bytes(int block_axis, int64_t B, int64_t H, int64_t N, int64_t d) {
+    if (check_shape(B, H, N, d) != MXATTN_OK) return 0;
+    if (block_axis == MXATTN_AXIS_HEAD_DIM) return (size_t)(B * H * N * (d / 2));
+    if (block_axis == MXATTN_AXIS_TOKENS) return (size_t)(B * H * d * ((N + 31) / 32) * 16);
+    return 0;
+}
+
+size_t mxattn_scales_bytes(int block_axis, int64_t B, int64_t H, int64_t N, int64_t d) {
+    if (check_shape(B, H, N, d) != MXATTN_OK) return 0;
+    if (block_axis == MXATTN_AXIS_HEAD_DIM) return (size_t)(B * H * N * (d / 32));
+    if (block_axis == MXATTN_AXIS_TOKENS) return (size_t)(B * H * d * ((N + 31) / 32));
+    return 0;
+}
+
+int mxattn_quantize(const void* x, uint8_t* codes, uint8_t* scales, int block_axis, int mode,
+                    int64_t B, int64_t H, int64_t N, int64_t d, void* stream) {
+    if (!x || !codes || !scales) return MXATTN_ERR_NULL;
+    if (block_axis != MXATTN_AXIS_HEAD_DIM && block_axis != MXATTN_AXIS_TOKENS) return MXATTN_ERR_AXIS;
+    if (!valid_mode(mode)) return MXATTN_ERR_MODE;
+    if (int st = check_shape(B, H, N, d)) return st;
+    if (!aligned(x, 16) || !aligned(codes, 16)) return MXATTN_ERR_ALIGN;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    hipError_t e;
+    if (block_axis == MXATTN_AXIS_HEAD_DIM)
+        e = mxattn::launch_quantize_headdim(x, codes, scales, B * H * N, rule_of(mode), s);
+    else
+        e = mxattn::launch_quantize_tokens(x, codes, scales, B * H, N, rule_of(mode), s);
+    if (e != hipSuccess) {
+        set_error("quantize launch", e);
+        return MXATTN_ERR_HIP;
+    }
+    return MXATTN_OK;
+}
+
+static int launch_attend(const uint8_t* qc, const uint8_t* qs, const uint8_t* kc,
+                         const uint8_t* ks, const uint8_t* vc, const uint8_t* vs, void* out,
+                         int64_t B, int64_t H, int64_t N, int mode, hipStream_t s) {
+    mxattn::AttnArgs a;
+    a.qc = qc;
+    a.qs = qs;
+    a.kc = kc;
+    a.ks = ks;
+    a.vc = vc;
+    a.vs = vs;
+    a.out = static_cast<uint16_t*>(out);
+    a.N = (int)N;
+    a.nb = (int)((N + 31) / 32);
+    a.qtiles = (int)((N + mxattn::kQueryTile - 1) / mxattn::kQueryTile);
+    const int64_t total = B * H * a.qtiles;
+    if (total > (int64_t)1 << 30) return MXATTN_ERR_SHAPE;
+    a.total_tiles = (int)total;
+    a.per_xcd = (int)((total + 7) / 8);
+    hipError_t e = mxattn::launch_attention(a, mode, s);
+    if (e != hipSuccess) {
+        set_error("attention launch", e);
+        return MXATTN_ERR_HIP;
+    }
+    return MXATTN_OK;
+}
+
+int mxattn_attend(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
+                  const uint8_t* k_scales, const uint8_t* v_codes, const uint8_t* v_scales,
+                  void* out, int64_t B, int64_t H, int64_t N, int64_t d, int mode, void* stream) {
+    if (!q_codes || !q_scales || !k_codes || !k_scales || !v_codes || !v_scales || !out)
+        return MXATTN_ERR_NULL;
+    if (!valid_mode(mode)) return MXATTN_ERR_MODE;
+    if (int st = check_shape(B, H, N, d)) return st;
+    if (!aligned(q_codes, 16) || !aligned(k_codes, 16) || !aligned(v_codes, 16) ||
+        !aligned(out, 16) || !aligned(k_scales, 4))
+        return MXATTN_ERR_ALIGN;
+    return launch_attend(q_codes, q_scales, k_codes, k_scales, v_codes, v_scales, out, B, H, N,
+                         mode, reinterpret_cast<hipStream_t>(stream));
+}
+
+int mxattn_forward(const void* q, const void* k, const void* v, void* out, int64_t B, int64_t H,
+                   int64_t N, int64_t d, int mode, void* stream) {
+    if (!q || !k || !v || !out) return MXATTN_ERR_NULL;
+    if (!valid_mode(mode)) return MXATTN_ERR_MODE;
+    if (int st = check_shape(B, H, N, d)) return st;
+    if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16))
+        return MXATTN_ERR_ALIGN;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    keep_pool_memory();
+
+    const size_t qk_codes = mxattn_codes_bytes(MXATTN_AXIS_HEAD_DIM, B, H, N, d);
+    const size_t qk_scales = mxattn_scales_bytes(MXATTN_AXIS_HEAD_DIM, B, H, N, d);
+    const size_t v_codes = mxattn_codes_bytes(MXATTN_AXIS_TOKENS, B, H, N, d);
+    const size_t v_scales = mxattn_scales_bytes(MXATTN_AXIS_TOKENS, B, H, N, d);
+    auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    const size_t total = 2 * up(qk_codes) + 2 * up(qk_scales) + up(v_codes) + up(v_scales);
+
+    void* ws = nullptr;
+    hipError_t e = hipMallocAsync(&ws, total, s);
+    if (e != hipSuccess || !ws) {
+        set_error("hipMallocAsync", e);
+        return MXATTN_ERR_OOM;
+    }
+    uint8_t* p = static_cast<uint8_t*>(ws);
+    uint8_t* qc = p;
+    p += up(qk_codes);
+    uint8_t* kc = p;
+    p += up(qk_codes);
+    uint8_t* vc = p;
+    p += up(v_codes);
+    uint8_t* qs = p;
+    p += up(qk_scales);
+    uint8_t* ks = p;
+    p += up(qk_scales);
+    uint8_t* vs = p;
+
+    const int rule = rule_of(mode);
+    int st = MXATTN_OK;
+    if ((e = mxattn::launch_quantize_headdim(q, qc, qs, B * H * N, rule, s)) != hipSuccess ||
+        (e = mxattn::launch_quantize_headdim(k, kc, ks, B * H * N, rule, s)) != hipSuccess ||
+        (e = mxattn::launch_quantize_tokens(v, vc, vs, B * H, N, rule, s)) != hipSuccess) {
+        set_error("quantize launch", e);
+        st = MXATTN_ERR_HIP;
+    } else {
+        st = launch_attend(qc, qs, kc, ks, vc, vs, out, B, H, N, mode, s);
+    }
+    e = hipFreeAsync(ws, s);
+    if (st == MXATTN_OK && e != hipSuccess) {
+        set_error("hipFreeAsync", e);
+        st = MXATTN_ERR_HIP;
+    }
+    return st;
+}
+
+}  // extern "C"

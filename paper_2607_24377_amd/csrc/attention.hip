@@ -1,0 +1,342 @@
+// attention.hip -- fused MXFP4 flash attention forward for gfx950.
+//
+// One workgroup = 4 waves = 128 query rows of one (batch, head); each wave
+// owns 32 query rows.  The kernel walks the keys in tiles of 128 (the KV tile
+// B_c) in increasing order, as Algorithm 2 does, and for each tile:
+//
+//   1. stages the MXFP4 K^ and V^ codes and E8M0 scales of the tile in LDS;
+//   2. S^T = K^ Q^T on the block-scaled FP4 matrix cores
+//      (V_MFMA_SCALE_F32_32X32X64_F8F6F4, fp32 accumulation);
+//   3. online softmax in registers: running maximum m, correction
+//      alpha = exp2(m_old - m_new), P~ = exp2(s*c - m_new) with
+//      c = log2(e)/sqrt(d)  (Sec. 2, Eq. online_attention);
+//   4. quantizes P~ in 32-key blocks in registers with the mode's scale rule
+//      straight into the FP4 operand layout of the PV product (Algorithm 2,
+//      P^ = Q*(P~));
+//   5. l = alpha*l + sum(P~) (direct placement, Eq. direct_mxfp4_tile) or
+//      l = alpha*l + sum(P^) (PNQ, Eq. pnq_online_update);  the PNQ row sum
+//      of the dequantized P^ is taken on the matrix cores as ones * P^T;
+//   6. O~^T = diag(alpha) O~^T + V^T P^T on the FP4 matrix cores.
+//
+// After the last tile O = O~ / l is rounded to bf16 (Eq.
+// online_attention_output).
+//
+// Layouts chosen so that no lane shuffles are needed between the two
+// products: with S^T (keys as rows) each lane holds the scores of ONE query
+// for 16 keys of a 32x32 tile.  The key order of the K^ rows fed to the S
+// product is permuted so that after two tiles (64 keys) lane (query q,
+// half h) holds exactly keys 32h..32h+31 of that 64-key chunk in natural
+// order: one complete MXFP4 block of P~, which is both the unit of the P~
+// quantization and the B-operand layout of the 32x32x64 PV product.
+//
+// Arithmetic contract (mirrored by the CPU oracle):
+//   s     fp32 accumulation of exact FP4 products (matrix core)
+//   m'    max(m', RD(c * max s)), RD = largest fp32 <= the exact product
+//   t     fmaf(s, c, -m')
+//   P~    v_exp_f32(t): faithful (<1 ulp), flushes results below 2^-126
+//   scale from the block maximum of P~ (exp2 of the block's largest t)
+//   P^    the gfx950 FP4 conversion of P~ / 2^e (round to nearest, ties to
+//         the even code, saturating)
+#include "device_common.h"
+#include "launch.h"
+
+namespace mxattn {
+namespace {
+
+constexpr int kWaves = 4;
+constexpr int kThreads = kWaves * 64;
+constexpr int kQw = 32;  // query rows per wave
+
+// LDS stage layout (bytes)
+constexpr int kKcOff = 0;      // K^ codes: 128 rows x 64 B, rows in MFMA order
+constexpr int kKsOff = 8192;   // K^ scales: 64 lanes x 8 B, pre-permuted per lane
+constexpr int kVcOff = 8704;   // V^ codes: 128 rows (channels) x 64 B (128 keys)
+constexpr int kVsOff = 16896;  // V^ scales: 64 lanes x 8 B
+constexpr int kStageBytes = 17408;
+
+// 16-byte slot swizzle of a 64-byte LDS row: any 16 consecutive rows read at
+// the same logical slot hit 16 distinct 16-byte bank groups.
+__device__ __forceinline__ int swz(int row) { return ((row >> 1) ^ (row >> 2)) & 3; }
+
+// Row of the K^ tile (in MFMA order) that holds key w (0..63) of a 64-key
+// chunk: tile j = bit 4 of w, A-row r = 8*(w bits 2-3) + 4*(w bit 5) + (w & 3).
+// In the 32x32 output layout, accumulator i of lane (q, h) is A-row
+// 8*(i/4) + 4*h + (i%4), so lane (q, h) receives key 32*h + 16*j + i.
+__device__ __forceinline__ void key_slot(int w, int& j, int& r) {
+    j = (w >> 4) & 1;
+    r = 8 * ((w >> 2) & 3) + 4 * ((w >> 5) & 1) + (w & 3);
+}
+
+__device__ __forceinline__ void stage_tile(uint8_t* lds, const AttnArgs& a, int bh, int tile,
+                                           int tid) {
+    const int N = a.N, nb = a.nb;
+    const int k0 = tile * 128;
+    const int64_t krow0 = (int64_t)bh * N;
+    // K^ codes: 128 keys x 4 chunks of 16 B (keys past N read the last key;
+    // their scores are masked)
+#pragma unroll
+    for (int it = 0; it < 2; it++) {
+        const int idx = tid + kThreads * it;
+        const int key = idx >> 2, db = idx & 3;
+        const int gk = min(k0 + key, N - 1);
+        const uint4 v = *reinterpret_cast<const uint4*>(a.kc + (krow0 + gk) * 64 + db * 16);
+        int j, r;
+        key_slot(key & 63, j, r);
+        const int row = 64 * (key >> 6) + 32 * j + r;
+        *reinterpret_cast<uint4*>(lds + kKcOff + row * 64 + 16 * (db ^ swz(row))) = v;
+    }
+    // K^ scales: lane (r + 32*(db&1)) of S product (chunk c, tile j, half db>>1)
+    if (tid < 128) {
+        const int key = tid;
+        const int gk = min(k0 + key, N - 1);
+        const uint32_t s4 = *reinterpret_cast<const uint32_t*>(a.ks + (krow0 + gk) * 4);
+        int j, r;
+        key_slot(key & 63, j, r);
+        const int c = key >> 6;
+#pragma unroll
+        for (int db = 0; db < 4; db++) {
+            const int lane = r + 32 * (db & 1);
+            lds[kKsOff + lane * 8 + c * 4 + j * 2 + (db >> 1)] = (uint8_t)(s4 >> (8 * db));
+        }
+    }
+    // V^ codes: 128 channel rows x 4 key blocks of 16 B (blocks past the end
+    // read the last block; the matching P^ entries are zero)
+    const int64_t vrow0 = (int64_t)bh * 128;
+#pragma unroll
+    for (int it = 0; it < 2; it++) {
+        const int idx = tid + kThreads * it;
+        const int d = idx >> 2, kb = idx & 3;
+        const int blk = min(4 * tile + kb, nb - 1);
+        const uint4 v =
+            *reinterpret_cast<const uint4*>(a.vc + ((vrow0 + d) * nb + blk) * 16);
+        *reinterpret_cast<uint4*>(lds + kVcOff + d * 64 + 16 * (kb ^ swz(d))) = v;
+    }
+    // V^ scales: lane (d%32 + 32*(kb&1)) of PV product (channel tile d/32,
+    // chunk kb>>1)
+    if (tid < 128) {
+        const int d = tid;
+#pragma unroll
+        for (int kb = 0; kb < 4; kb++) {
+            const int blk = min(4 * tile + kb, nb - 1);
+            const uint8_t s = a.vs[(vrow0 + d) * nb + blk];
+            const int lane = (d & 31) + 32 * (kb & 1);
+            lds[kVsOff + lane * 8 + (d >> 5) * 2 + (kb >> 1)] = s;
+        }
+    }
+}
+
+template <int kScaleOpsel>
+__device__ __forceinline__ v16f mfma_fp4(v8i a, v8i b, v16f c, int sa, int sb) {
+    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 4, 4, kScaleOpsel, sa, 0, sb);
+}
+
+template <int kRule, bool kPnq>
+__global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
+    __shared__ __attribute__((aligned(16))) uint8_t lds[kStageBytes];
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6, lane = tid & 63;
+    const int q = lane & 31, h = lane >> 5;
+
+    // XCD-aware order: consecutive workgroup ids go round-robin over the 8
+    // XCDs, so give each XCD a contiguous range of (head, query tile) work;
+    // the workgroups sharing an L2 then stream the same head's K^/V^.
+    const int L = blockIdx.x;
+    const int logical = (L & 7) * a.per_xcd + (L >> 3);
+    if (logical >= a.total_tiles) return;
+    const int bh = logical / a.qtiles;
+    const int qt = logical - bh * a.qtiles;
+    const int N = a.N;
+    const int64_t rowbase = (int64_t)bh * N;
+    const int qi = qt * kQueryTile + wave * kQw + q;
+    const int qic = min(qi, N - 1);
+
+    // Q^ as the B operand of S^T = K^ Q^T: lane (q, h) holds channel block
+    // 2*hf + h of its query for the product over channels 64*hf..64*hf+63.
+    const uint8_t* qrow = a.qc + (rowbase + qic) * 64;
+    const v8i qB0 = fp4_operand(*reinterpret_cast<const uint4*>(qrow + 16 * h));
+    const v8i qB1 = fp4_operand(*reinterpret_cast<const uint4*>(qrow + 16 * (2 + h)));
+    const int qS0 = a.qs[(rowbase + qic) * 4 + h];
+    const int qS1 = a.qs[(rowbase + qic) * 4 + 2 + h];
+
+    // FP4 1.0 (code 0b0010) in every position: ones * P^T gives the row sums
+    v8i ones;
+#pragma unroll
+    for (int i = 0; i < 8; i++) ones[i] = i < 4 ? 0x22222222 : 0;
+
+    const float cl = 0.12751743082459868f;  // fp32(log2(e) / sqrt(128))
+    float m = -__builtin_inff();
+    float lacc = 0.f;
+    v16f O[4];
+#pragma unroll
+    for (int n = 0; n < 4; n++)
+#pragma unroll
+        for (int i = 0; i < 16; i++) O[n][i] = 0.f;
+
+    const int ntiles = (N + 127) / 128;
+    for (int tile = 0; tile < ntiles; tile++) {
+        __syncthreads();
+        stage_tile(lds, a, bh, tile, tid);
+        __syncthreads();
+
+        const uint2 ksb = *reinterpret_cast<const uint2*>(lds + kKsOff + lane * 8);
+        const uint2 vsb = *reinterpret_cast<const uint2*>(lds + kVsOff + lane * 8);
+
+        // ---- S^T = K^ Q^T: S[c][j][i] is key 64c + 32h + 16j + i of the tile
+        v16f S[2][2];
+#pragma unroll
+        for (int c = 0; c < 2; c++) {
+#pragma unroll
+            for (int j = 0; j < 2; j++) {
+                const int row = 64 * c + 32 * j + q;
+                const uint8_t* rp = lds + kKcOff + row * 64;
+                const int sw = swz(row);
+                const v8i k0v = fp4_operand(*reinterpret_cast<const uint4*>(rp + 16 * ((0 + h) ^ sw)));
+                const v8i k1v = fp4_operand(*reinterpret_cast<const uint4*>(rp + 16 * ((2 + h) ^ sw)));
+                const int sreg = c == 0 ? (int)ksb.x : (int)ksb.y;
+                v16f acc;
+#pragma unroll
+                for (int i = 0; i < 16; i++) acc[i] = 0.f;
+                if (j == 0) {
+                    acc = mfma_fp4<0>(k0v, qB0, acc, sreg, qS0);
+                    acc = mfma_fp4<1>(k1v, qB1, acc, sreg, qS1);
+                } else {
+                    acc = mfma_fp4<2>(k0v, qB0, acc, sreg, qS0);
+                    acc = mfma_fp4<3>(k1v, qB1, acc, sreg, qS1);
+                }
+                S[c][j] = acc;
+            }
+        }
+
+        // ---- mask keys past the end of the sequence (last tile only)
+        const int k0 = tile * 128;
+        if (k0 + 128 > N) {
+#pragma unroll
+            for (int c = 0; c < 2; c++)
+#pragma unroll
+                for (int j = 0; j < 2; j++)
+#pragma unroll
+                    for (int i = 0; i < 16; i++)
+                        if (k0 + 64 * c + 32 * h + 16 * j + i >= N) S[c][j][i] = -__builtin_inff();
+        }
+
+        // ---- running maximum
+        float bmax[2];
+#pragma unroll
+        for (int c = 0; c < 2; c++) {
+            float mx = S[c][0][0];
+#pragma unroll
+            for (int j = 0; j < 2; j++)
+#pragma unroll
+                for (int i = 0; i < 16; i++) mx = fmaxf(mx, S[c][j][i]);
+            bmax[c] = mx;
+        }
+        float rmax = fmaxf(bmax[0], bmax[1]);
+        rmax = fmaxf(rmax, __shfl_xor(rmax, 32));
+        float u = cl * rmax;
+        if (__builtin_fmaf(rmax, cl, -u) < 0.f) u = next_down(u);  // RD(c * max s)
+        const float m_new = fmaxf(m, u);
+        const float alpha = __builtin_amdgcn_exp2f(m - m_new);  // 0 on the first tile
+        m = m_new;
+
+        // ---- P~, its MXFP4 quantization P^, row-sum contribution
+        v8i P[2];
+        int psc[2];
+        float lsum = 0.f;
+#pragma unroll
+        for (int c = 0; c < 2; c++) {
+            const float mb = __builtin_amdgcn_exp2f(__builtin_fmaf(bmax[c], cl, -m_new));
+            const uint32_t mbits = __builtin_bit_cast(uint32_t, mb);
+            const uint32_t sbyte =
+                (mbits < 0x00800000u) ? 127u : (uint32_t)(scale_exponent_f32<kRule>(mbits) + 127);
+            const float sf = e8m0_as_f32(sbyte);
+            psc[c] = (int)sbyte;
+            uint32_t w[4] = {0, 0, 0, 0};
+#pragma unroll
+            for (int n = 0; n < 32; n += 2) {
+                const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(S[c][n >> 4][n & 15], cl, -m_new));
+                const float p1 =
+                    __builtin_amdgcn_exp2f(__builtin_fmaf(S[c][(n + 1) >> 4][(n + 1) & 15], cl, -m_new));
+                if (!kPnq) lsum += p0 + p1;
+                const int wd = n >> 3;
+                switch ((n & 7) >> 1) {
+                    case 0: w[wd] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w[wd], p0, p1, sf, 0); break;
+                    case 1: w[wd] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w[wd], p0, p1, sf, 1); break;
+                    case 2: w[wd] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w[wd], p0, p1, sf, 2); break;
+                    default: w[wd] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w[wd], p0, p1, sf, 3); break;
+                }
+            }
+            P[c] = fp4_operand(make_uint4(w[0], w[1], w[2], w[3]));
+        }
+
+        float dl;
+        if (kPnq) {
+            v16f lt;
+#pragma unroll
+            for (int i = 0; i < 16; i++) lt[i] = 0.f;
+            lt = mfma_fp4<0>(ones, P[0], lt, 127, psc[0]);
+            lt = mfma_fp4<0>(ones, P[1], lt, 127, psc[1]);
+            dl = lt[0];
+        } else {
+            dl = lsum;  // this lane's half of the row; halves are added at the end
+        }
+        lacc = alpha * lacc + dl;
+
+        // ---- O~^T = diag(alpha) O~^T + V^T P^T
+        if (__any(alpha != 1.f)) {
+#pragma unroll
+            for (int n = 0; n < 4; n++)
+#pragma unroll
+                for (int i = 0; i < 16; i++) O[n][i] *= alpha;
+        }
+#pragma unroll
+        for (int n = 0; n < 4; n++) {
+            const int row = 32 * n + q;
+            const uint8_t* rp = lds + kVcOff + row * 64;
+            const int sw = swz(row);
+            const v8i v0 = fp4_operand(*reinterpret_cast<const uint4*>(rp + 16 * ((0 + h) ^ sw)));
+            const v8i v1 = fp4_operand(*reinterpret_cast<const uint4*>(rp + 16 * ((2 + h) ^ sw)));
+            const int sreg = n < 2 ? (int)vsb.x : (int)vsb.y;
+            // scale byte index 2n + c within the lane's 8 bytes
+            if ((n & 1) == 0) {
+                O[n] = mfma_fp4<0>(v0, P[0], O[n], sreg, psc[0]);
+                O[n] = mfma_fp4<1>(v1, P[1], O[n], sreg, psc[1]);
+            } else {
+                O[n] = mfma_fp4<2>(v0, P[0], O[n], sreg, psc[0]);
+                O[n] = mfma_fp4<3>(v1, P[1], O[n], sreg, psc[1]);
+            }
+        }
+    }
+
+    // ---- O = O~ / l  -> bf16
+    float ltot = lacc;
+    if (!kPnq) ltot += __shfl_xor(lacc, 32);
+    if (qi < N) {
+        uint16_t* orow = a.out + (int64_t)(rowbase + qi) * 128;
+#pragma unroll
+        for (int n = 0; n < 4; n++) {
+#pragma unroll
+            for (int g = 0; g < 4; g++) {
+                const uint32_t b0 = f32_to_bf16_bits(O[n][4 * g + 0] / ltot);
+                const uint32_t b1 = f32_to_bf16_bits(O[n][4 * g + 1] / ltot);
+                const uint32_t b2 = f32_to_bf16_bits(O[n][4 * g + 2] / ltot);
+                const uint32_t b3 = f32_to_bf16_bits(O[n][4 * g + 3] / ltot);
+                *reinterpret_cast<uint2*>(orow + 32 * n + 8 * g + 4 * h) =
+                    make_uint2(b0 | (b1 << 16), b2 | (b3 << 16));
+            }
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_attention(const AttnArgs& a, int mode, hipStream_t stream) {
+    const dim3 grid((unsigned)(8 * a.per_xcd));
+    switch (mode) {
+        case 0: attention_kernel<kRuleOcp, false><<<grid, kThreads, 0, stream>>>(a); break;
+        case 1: attention_kernel<kRuleUos, false><<<grid, kThreads, 0, stream>>>(a); break;
+        default: attention_kernel<kRuleUos, true><<<grid, kThreads, 0, stream>>>(a); break;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace mxattn

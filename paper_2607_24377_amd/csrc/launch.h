@@ -1,0 +1,40 @@
+// launch.h -- host-side launchers of the libmxattn kernels (internal).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mxattn {
+
+// Shared-scale rule of the MXFP4 quantizer.
+enum Rule { kRuleOcp = 0, kRuleUos = 1 };
+
+// Query rows per workgroup and keys per KV tile of the fused attention kernel.
+constexpr int kQueryTile = 128;
+constexpr int kKvTile = 128;
+
+hipError_t launch_quantize_headdim(const void* x, uint8_t* codes, uint8_t* scales, int64_t rows,
+                                   int rule, hipStream_t stream);
+
+hipError_t launch_quantize_tokens(const void* x, uint8_t* codes, uint8_t* scales, int64_t BH,
+                                  int64_t N, int rule, hipStream_t stream);
+
+struct AttnArgs {
+    const uint8_t* qc;  // [BH, N, 64]
+    const uint8_t* qs;  // [BH, N, 4]
+    const uint8_t* kc;  // [BH, N, 64]
+    const uint8_t* ks;  // [BH, N, 4]
+    const uint8_t* vc;  // [BH, 128, nb * 16]
+    const uint8_t* vs;  // [BH, 128, nb]
+    uint16_t* out;      // [BH, N, 128] bf16
+    int N;
+    int nb;
+    int qtiles;
+    int total_tiles;
+    int per_xcd;
+};
+
+// mode: 0 OCP + direct, 1 UOS + direct, 2 UOS + PNQ
+hipError_t launch_attention(const AttnArgs& a, int mode, hipStream_t stream);
+
+}  // namespace mxattn

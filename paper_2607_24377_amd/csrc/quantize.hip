@@ -1,0 +1,169 @@
+// quantize.hip -- MXFP4 block quantizers for gfx950 (Algorithm 1 with the UOS
+// or the OCP floor scale rule).
+//
+// Both kernels stream bf16 from HBM once and write 4-bit codes plus one E8M0
+// byte per 32 elements (2.53125 bytes of traffic per element).  The E2M1
+// rounding itself is done by the gfx950 scaled FP4 conversion, which rounds to
+// nearest with ties to the even code, saturates at +-6 and keeps the sign bit
+// (the same readings the library documents for the quantizer).
+#include "device_common.h"
+#include "launch.h"
+
+namespace mxattn {
+
+// ---------------------------------------------------------------------------
+// Blocks along the head dimension (Q and K).  Each thread owns 8 consecutive
+// elements (one 16-byte load); the 4 threads of a 32-element block are
+// adjacent lanes and exchange their maxima with two lane swaps.
+// ---------------------------------------------------------------------------
+template <int kRule>
+__global__ __launch_bounds__(256) void quantize_headdim_kernel(const uint4* __restrict__ x,
+                                                               uint32_t* __restrict__ codes,
+                                                               uint8_t* __restrict__ scales,
+                                                               int64_t n_chunks) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const bool valid = i < n_chunks;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (valid) v = x[i];
+
+    // block maximum of |x| on the bf16 bit patterns (order-preserving for
+    // nonnegative finite values)
+    uint32_t m = 0;
+    m = max(m, v.x & 0x7FFFu);
+    m = max(m, (v.x >> 16) & 0x7FFFu);
+    m = max(m, v.y & 0x7FFFu);
+    m = max(m, (v.y >> 16) & 0x7FFFu);
+    m = max(m, v.z & 0x7FFFu);
+    m = max(m, (v.z >> 16) & 0x7FFFu);
+    m = max(m, v.w & 0x7FFFu);
+    m = max(m, (v.w >> 16) & 0x7FFFu);
+    m = max(m, (uint32_t)__shfl_xor((int)m, 1));
+    m = max(m, (uint32_t)__shfl_xor((int)m, 2));
+
+    // all-zero block: sigma = 1 (Algorithm 1); codes come out as signed zeros
+    const uint32_t sbyte = (m == 0) ? 127u : (uint32_t)(scale_exponent_bf16<kRule>(m) + 127);
+    const float sf = e8m0_as_f32(sbyte);
+
+    uint32_t c = 0;
+    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c, __builtin_bit_cast(bf16x2, v.x), sf, 0);
+    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c, __builtin_bit_cast(bf16x2, v.y), sf, 1);
+    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c, __builtin_bit_cast(bf16x2, v.z), sf, 2);
+    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c, __builtin_bit_cast(bf16x2, v.w), sf, 3);
+    if (valid) {
+        codes[i] = c;
+        if ((i & 3) == 0) scales[i >> 2] = (uint8_t)sbyte;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Blocks along the token axis (V).  A workgroup stages 128 tokens x 128
+// channels of one head (32 KiB of bf16) in LDS with coalesced 16-byte loads;
+// wave w then quantizes token block w of the group, each lane owning a pair
+// of channels.  Tokens past N are staged as +0 (the zero padding of the last
+// block).  Output rows are tokens-contiguous per channel: 16 code bytes and
+// one scale byte per (channel, 32-token block).
+// ---------------------------------------------------------------------------
+constexpr int kVqTokens = 128;
+
+template <int kRule>
+__global__ __launch_bounds__(256) void quantize_tokens_kernel(const uint4* __restrict__ x,
+                                                              uint8_t* __restrict__ codes,
+                                                              uint8_t* __restrict__ scales, int N,
+                                                              int nb, int groups) {
+    __shared__ uint32_t tile[kVqTokens * 64];  // [token][64 dwords = 128 bf16]
+    const int tid = threadIdx.x;
+    const int bh = blockIdx.x / groups;
+    const int g = blockIdx.x % groups;
+    const int tok0 = g * kVqTokens;
+
+    const uint4* src = x + (int64_t)bh * N * 16;  // 16 chunks of 16 B per token
+#pragma unroll
+    for (int k = 0; k < 8; k++) {
+        int ch = tid + 256 * k;  // chunk id within the group
+        int tok = ch >> 4, part = ch & 15;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (tok0 + tok < N) v = src[(int64_t)(tok0 + tok) * 16 + part];
+        *reinterpret_cast<uint4*>(&tile[tok * 64 + part * 4]) = v;
+    }
+    __syncthreads();
+
+    const int w = tid >> 6;   // token block within the group
+    const int cp = tid & 63;  // channels 2cp, 2cp+1
+    const int blk = 4 * g + w;
+    if (blk >= nb) return;
+
+    uint32_t col[32];
+    uint32_t m0 = 0, m1 = 0;
+#pragma unroll
+    for (int t = 0; t < 32; t++) {
+        uint32_t d = tile[(32 * w + t) * 64 + cp];
+        col[t] = d;
+        m0 = max(m0, d & 0x7FFFu);
+        m1 = max(m1, (d >> 16) & 0x7FFFu);
+    }
+    const uint32_t s0 = (m0 == 0) ? 127u : (uint32_t)(scale_exponent_bf16<kRule>(m0) + 127);
+    const uint32_t s1 = (m1 == 0) ? 127u : (uint32_t)(scale_exponent_bf16<kRule>(m1) + 127);
+    const float f0 = e8m0_as_f32(s0), f1 = e8m0_as_f32(s1);
+
+    uint32_t c0[4] = {0, 0, 0, 0}, c1[4] = {0, 0, 0, 0};
+#pragma unroll
+    for (int t = 0; t < 32; t += 2) {
+        // (token t, token t+1) pairs of each channel
+        uint32_t lo = __builtin_amdgcn_perm(col[t + 1], col[t], 0x05040100u);  // low halves
+        uint32_t hi = __builtin_amdgcn_perm(col[t + 1], col[t], 0x07060302u);  // high halves
+        const int word = t >> 3, sel = (t & 7) >> 1;
+        switch (sel) {
+            case 0:
+                c0[word] = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c0[word], __builtin_bit_cast(bf16x2, lo), f0, 0);
+                c1[word] = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c1[word], __builtin_bit_cast(bf16x2, hi), f1, 0);
+                break;
+            case 1:
+                c0[word] = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c0[word], __builtin_bit_cast(bf16x2, lo), f0, 1);
+                c1[word] = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c1[word], __builtin_bit_cast(bf16x2, hi), f1, 1);
+                break;
+            case 2:
+                c0[word] = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c0[word], __builtin_bit_cast(bf16x2, lo), f0, 2);
+                c1[word] = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c1[word], __builtin_bit_cast(bf16x2, hi), f1, 2);
+                break;
+            default:
+                c0[word] = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c0[word], __builtin_bit_cast(bf16x2, lo), f0, 3);
+                c1[word] = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c1[word], __builtin_bit_cast(bf16x2, hi), f1, 3);
+                break;
+        }
+    }
+    const int64_t row0 = (int64_t)bh * 128 + 2 * cp;
+    *reinterpret_cast<uint4*>(codes + (row0 * nb + blk) * 16) = make_uint4(c0[0], c0[1], c0[2], c0[3]);
+    *reinterpret_cast<uint4*>(codes + ((row0 + 1) * nb + blk) * 16) = make_uint4(c1[0], c1[1], c1[2], c1[3]);
+    scales[row0 * nb + blk] = (uint8_t)s0;
+    scales[(row0 + 1) * nb + blk] = (uint8_t)s1;
+}
+
+hipError_t launch_quantize_headdim(const void* x, uint8_t* codes, uint8_t* scales, int64_t rows,
+                                   int rule, hipStream_t stream) {
+    const int64_t n_chunks = rows * 16;  // d = 128: 16 chunks of 8 elements per row
+    if (n_chunks == 0) return hipSuccess;
+    const dim3 grid((unsigned)((n_chunks + 255) / 256));
+    if (rule == kRuleUos)
+        quantize_headdim_kernel<kRuleUos><<<grid, 256, 0, stream>>>(
+            (const uint4*)x, (uint32_t*)codes, scales, n_chunks);
+    else
+        quantize_headdim_kernel<kRuleOcp><<<grid, 256, 0, stream>>>(
+            (const uint4*)x, (uint32_t*)codes, scales, n_chunks);
+    return hipGetLastError();
+}
+
+hipError_t launch_quantize_tokens(const void* x, uint8_t* codes, uint8_t* scales, int64_t BH,
+                                  int64_t N, int rule, hipStream_t stream) {
+    const int nb = (int)((N + 31) / 32);
+    const int groups = (int)((N + kVqTokens - 1) / kVqTokens);
+    const dim3 grid((unsigned)(BH * groups));
+    if (rule == kRuleUos)
+        quantize_tokens_kernel<kRuleUos><<<grid, 256, 0, stream>>>((const uint4*)x, codes, scales,
+                                                                    (int)N, nb, groups);
+    else
+        quantize_tokens_kernel<kRuleOcp><<<grid, 256, 0, stream>>>((const uint4*)x, codes, scales,
+                                                                    (int)N, nb, groups);
+    return hipGetLastError();
+}
+
+}  // namespace mxattn

@@ -1,0 +1,173 @@
+"""GPU attention forward vs the CPU oracle fed the GPU's own codes.
+
+Tolerance (attention output, bf16 vs bf16): rel-L2 <= 2e-3 and max-abs <= 1e-2.
+The oracle mirrors the kernel's KV tile width and fp32 rounding points; the
+remaining differences are v_exp_f32's faithful (not always correctly rounded)
+exponential, which can move an element of P~ across an E2M1 decision
+threshold, and fp32 vs fp64 accumulation.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from parity import (MAX_ABS_TOL, REL_L2_TOL, flat, log, max_abs, oracle_rows, rel_l2,
+                    sample_rows, workload_bits)
+from paper_2607_24377_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+MODES = ["ocp_vanilla", "uos", "uos_pnq"]
+
+
+@pytest.fixture(scope="module")
+def mx():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2607_24377_amd import mxattn
+
+    mxattn.lib()
+    return mxattn
+
+
+def _gpu_codes(mx, qt, kt, vt, mode):
+    qc, qs = mx.quantize(qt, mx.AXIS_HEAD_DIM, mode)
+    kc, ks = mx.quantize(kt, mx.AXIS_HEAD_DIM, mode)
+    vc, vs = mx.quantize(vt, mx.AXIS_TOKENS, mode)
+    return {n: flat(t.cpu().numpy()) for n, t in
+            dict(qc=qc, qs=qs, kc=kc, ks=ks, vc=vc, vs=vs).items()}
+
+
+def _check_rows(mx, q, k, v, mode, heads_rows, N, label):
+    """Run the forward on the GPU and compare the given (head, rows) with the oracle."""
+    qt, kt, vt = (mx.bf16_from_bits(x) for x in (q, k, v))
+    out = mx.forward(qt, kt, vt, mode)
+    torch.cuda.synchronize()
+    codes = _gpu_codes(mx, qt, kt, vt, mode)
+    got_all = flat(mx.bits_from_bf16(out))
+    bc = mx.kv_tile()
+    worst = (0.0, 0.0)
+    gots, refs = [], []
+    for head, rows in heads_rows:
+        ref, _ = oracle_rows(codes, head, N, rows, mode, bc)
+        got = oracle.bf16_to_f64(got_all[head][rows])
+        gots.append(got)
+        refs.append(ref)
+        worst = (max(worst[0], rel_l2(got, ref)), max(worst[1], max_abs(got, ref)))
+    g = np.concatenate(gots)
+    r = np.concatenate(refs)
+    rl, ma = rel_l2(g, r), max_abs(g, r)
+    log(f"[attn] {label} mode={mode}: rel-L2 {rl:.3e} max-abs {ma:.3e} (worst head {worst[0]:.3e})")
+    assert np.all(np.isfinite(g))
+    assert rl <= REL_L2_TOL, (label, mode, rl)
+    assert ma <= MAX_ABS_TOL, (label, mode, ma)
+    return out
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_tiny_all_rows(mx, mode):
+    w = inputs.workload(0)
+    q, k, v = workload_bits(0)
+    hr = [(h, np.arange(w.N)) for h in range(w.B * w.H)]
+    _check_rows(mx, q, k, v, mode, hr, w.N, w.name)
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_outlier_channels_sampled(mx, mode):
+    w = inputs.workload(1)
+    q, k, v = workload_bits(1)
+    heads = [0, 7, 19, 39]
+    hr = [(h, sample_rows(w.N, 48, 100 + h)) for h in heads]
+    _check_rows(mx, q, k, v, mode, hr, w.N, w.name)
+
+
+@pytest.mark.parametrize("cfg", [2, 3, 4])
+def test_video_workloads_sampled(mx, cfg):
+    """Full-size video-DiT workloads, in the launch the benchmark times; the
+    oracle checks stratified sampled rows of several heads."""
+    w = inputs.workload(cfg)
+    q, k, v = workload_bits(cfg)
+    heads = [0, w.H // 2, w.B * w.H - 1]
+    for mode in MODES:
+        hr = [(h, sample_rows(w.N, 24, 1000 * cfg + h, w.text_tokens)) for h in heads]
+        _check_rows(mx, q, k, v, mode, hr, w.N, w.name)
+        torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("N", [1, 2, 31, 32, 33, 64, 127, 128, 129, 200, 255, 257, 640, 1001])
+def test_ragged_lengths(mx, N):
+    w = inputs.custom(2, 3, N, kind="video", index=50 + N % 7)
+    q, k, v = inputs.generate(w)
+    hr = [(h, np.arange(N)) for h in range(6)]
+    for mode in MODES:
+        _check_rows(mx, q, k, v, mode, hr, N, f"ragged N={N}")
+
+
+def test_v_all_ones(mx):
+    """V = 1 gives V^ = 1 exactly; PNQ returns exactly 1.0 and the direct modes
+    return the induced row sums (Eq. pnq_direct_full_rowsum)."""
+    w = inputs.custom(1, 2, 700, kind="iid", index=61)
+    q, k, _ = inputs.generate(w)
+    v = np.full_like(q, 0x3F80)  # bf16 1.0
+    qt, kt, vt = (mx.bf16_from_bits(x) for x in (q, k, v))
+    for mode in MODES:
+        out = mx.bits_from_bf16(mx.forward(qt, kt, vt, mode))
+        if mode == "uos_pnq":
+            assert np.all(out == 0x3F80)
+        else:
+            codes = _gpu_codes(mx, qt, kt, vt, mode)
+            for hd in range(2):
+                rows = np.arange(0, 700, 7)
+                ref, _, dg = oracle_rows(codes, hd, 700, rows, mode, mx.kv_tile(), diag=True)
+                got = oracle.bf16_to_f64(flat(out)[hd][rows])
+                np.testing.assert_allclose(got[:, 0], oracle.bf16_to_f64(oracle.round_bf16(dg[:, 1])),
+                                           rtol=8e-3)
+                assert np.mean(dg[:, 1]) < 1.0
+
+
+def test_identical_keys(mx):
+    """Identical keys make every P~ equal to 1 (up to ulps above 1), so P^ = 1
+    and O is the mean of the V^ rows in every mode."""
+    w = inputs.custom(1, 1, 300, kind="iid", index=62)
+    q, k, v = inputs.generate(w)
+    k[:] = k[:, :, :1, :]
+    qt, kt, vt = (mx.bf16_from_bits(x) for x in (q, k, v))
+    for mode in MODES:
+        out = oracle.bf16_to_f64(mx.bits_from_bf16(mx.forward(qt, kt, vt, mode)))[0, 0]
+        vc, vs = mx.quantize(vt, mx.AXIS_TOKENS, mode)
+        vh = oracle.dequant_keys(vc.cpu().numpy()[0, 0], vs.cpu().numpy()[0, 0], 300)
+        want = oracle.bf16_to_f64(oracle.round_bf16(vh.mean(0)))
+        assert max_abs(out, np.broadcast_to(want, out.shape)) <= 1e-2
+        assert rel_l2(out, np.broadcast_to(want, out.shape)) <= 4e-3
+
+
+def test_attend_matches_forward_and_is_deterministic(mx):
+    w = inputs.custom(2, 2, 1000, kind="video", index=63)
+    q, k, v = inputs.generate(w)
+    qt, kt, vt = (mx.bf16_from_bits(x) for x in (q, k, v))
+    for mode in MODES:
+        a = mx.forward(qt, kt, vt, mode)
+        b = mx.forward(qt, kt, vt, mode)
+        qc, qs = mx.quantize(qt, mx.AXIS_HEAD_DIM, mode)
+        kc, ks = mx.quantize(kt, mx.AXIS_HEAD_DIM, mode)
+        vc, vs = mx.quantize(vt, mx.AXIS_TOKENS, mode)
+        c = mx.attend(qc, qs, kc, ks, vc, vs, 1000, mode)
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+        assert torch.equal(a.view(torch.int16), c.view(torch.int16))
+
+
+def test_error_paths_leave_stream_usable(mx):
+    w = inputs.custom(1, 1, 64, kind="iid", index=64)
+    q, k, v = inputs.generate(w)
+    qt, kt, vt = (mx.bf16_from_bits(x) for x in (q, k, v))
+    L = mx.lib()
+    s = torch.cuda.current_stream().cuda_stream
+    assert L.mxattn_forward(qt.data_ptr(), kt.data_ptr(), vt.data_ptr(), None, 1, 1, 64, 128, 2, s) == 1
+    assert L.mxattn_forward(qt.data_ptr(), kt.data_ptr(), vt.data_ptr(), qt.data_ptr() + 2, 1, 1,
+                            64, 128, 2, s) == 3
+    assert L.mxattn_quantize(qt.data_ptr(), qt.data_ptr(), qt.data_ptr(), 4, 2, 1, 1, 64, 128, s) == 5
+    with pytest.raises(mx.MxattnError):
+        mx.forward(qt, kt, vt, 5)
+    out = mx.forward(qt, kt, vt, "uos_pnq")
+    torch.cuda.synchronize()
+    assert torch.isfinite(out.float()).all()
