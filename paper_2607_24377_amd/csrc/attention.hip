@@ -4,7 +4,9 @@
 // owns 32 query rows.  The kernel walks the keys in tiles of 128 (the KV tile
 // B_c) in increasing order, as Algorithm 2 does, and for each tile:
 //
-//   1. stages the MXFP4 K^ and V^ codes and E8M0 scales of the tile in LDS;
+//   1. reads the tile's MXFP4 K^ and V^ codes and E8M0 scales from LDS (the
+//      next tile is already being fetched from global memory into registers
+//      and lands in the other LDS buffer at the end of the iteration);
 //   2. S^T = K^ Q^T on the block-scaled FP4 matrix cores
 //      (V_MFMA_SCALE_F32_32X32X64_F8F6F4, fp32 accumulation);
 //   3. online softmax in registers: running maximum m, correction
@@ -29,6 +31,12 @@
 // order: one complete MXFP4 block of P~, which is both the unit of the P~
 // quantization and the B-operand layout of the 32x32x64 PV product.
 //
+// The softmax path (one FMA, one exp, half an FP4 conversion and half a
+// 3-way max per score) costs several times the matrix-core time of the two
+// products, so the kernel is VALU-bound; two workgroups per CU give each SIMD
+// two waves, and the matrix-core work of one hides under the softmax of the
+// other.
+//
 // Arithmetic contract (mirrored by the CPU oracle):
 //   s     fp32 accumulation of exact FP4 products (matrix core)
 //   m'    max(m', RD(c * max s)), RD = largest fp32 <= the exact product
@@ -47,7 +55,7 @@ constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr int kQw = 32;  // query rows per wave
 
-// LDS stage layout (bytes)
+// LDS stage layout (bytes); two stages
 constexpr int kKcOff = 0;      // K^ codes: 128 rows x 64 B, rows in MFMA order
 constexpr int kKsOff = 8192;   // K^ scales: 64 lanes x 8 B, pre-permuted per lane
 constexpr int kVcOff = 8704;   // V^ codes: 128 rows (channels) x 64 B (128 keys)
@@ -67,61 +75,80 @@ __device__ __forceinline__ void key_slot(int w, int& j, int& r) {
     r = 8 * ((w >> 2) & 3) + 4 * ((w >> 5) & 1) + (w & 3);
 }
 
-__device__ __forceinline__ void stage_tile(uint8_t* lds, const AttnArgs& a, int bh, int tile,
-                                           int tid) {
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef __attribute__((address_space(1))) void* gbl_ptr_t;
+
+// Global -> LDS copy of one tile's K^ and V^ codes (16 KiB) with the direct
+// gfx950 LDS loads: lane i of a wave-wide load writes the 16 bytes it fetched
+// to LDS base + 16*i, so each lane fetches whatever chunk belongs at its slot
+// of the permuted, swizzled layout.  Nothing passes through VGPRs; completion
+// is tracked by vmcnt.  Wave w copies LDS bytes [2048 w, 2048 w + 2048) of
+// each of the two 8 KiB code regions.
+__device__ __forceinline__ void load_tile_codes(uint8_t* st, const AttnArgs& a, int bh, int tile,
+                                                int wave, int lane) {
     const int N = a.N, nb = a.nb;
     const int k0 = tile * 128;
     const int64_t krow0 = (int64_t)bh * N;
-    // K^ codes: 128 keys x 4 chunks of 16 B (keys past N read the last key;
-    // their scores are masked)
+    const int64_t vrow0 = (int64_t)bh * 128;
 #pragma unroll
     for (int it = 0; it < 2; it++) {
-        const int idx = tid + kThreads * it;
-        const int key = idx >> 2, db = idx & 3;
-        const int gk = min(k0 + key, N - 1);
-        const uint4 v = *reinterpret_cast<const uint4*>(a.kc + (krow0 + gk) * 64 + db * 16);
-        int j, r;
-        key_slot(key & 63, j, r);
-        const int row = 64 * (key >> 6) + 32 * j + r;
-        *reinterpret_cast<uint4*>(lds + kKcOff + row * 64 + 16 * (db ^ swz(row))) = v;
+        const int p = (2 * wave + it) * 64 + lane;  // 16-byte slot of the region
+        const int row = p >> 2, slot = p & 3;
+        // K^: row -> (chunk c, tile j, A-row r) -> key; slot -> channel block
+        const int r = row & 31, j = (row >> 5) & 1, c = row >> 6;
+        const int key = 64 * c + 32 * ((r >> 2) & 1) + 16 * j + 4 * (r >> 3) + (r & 3);
+        const int gk = min(k0 + key, N - 1);  // keys past N: masked scores
+        const int db = slot ^ swz(row);
+        const uint8_t* ksrc = a.kc + (krow0 + gk) * 64 + db * 16;
+        __builtin_amdgcn_global_load_lds((gbl_ptr_t)ksrc, (lds_ptr_t)(st + kKcOff + (2 * wave + it) * 1024), 16, 0, 0);
+        // V^: row = channel, slot -> key block of the tile (blocks past the
+        // end read the last block; the matching P^ entries are zero)
+        const int kb = slot ^ swz(row);
+        const int blk = min(4 * tile + kb, nb - 1);
+        const uint8_t* vsrc = a.vc + ((vrow0 + row) * nb + blk) * 16;
+        __builtin_amdgcn_global_load_lds((gbl_ptr_t)vsrc, (lds_ptr_t)(st + kVcOff + (2 * wave + it) * 1024), 16, 0, 0);
     }
-    // K^ scales: lane (r + 32*(db&1)) of S product (chunk c, tile j, half db>>1)
+}
+
+// The tile's E8M0 scales in flight through registers: threads 0..127 hold
+// the 4 K^ scale bytes of key `tid`, threads 128..255 the 4 V^ scale bytes
+// of channel `tid - 128` (one byte per register, so no wait is needed until
+// they are written to LDS).
+struct TileScales {
+    uint32_t b[4];
+};
+
+__device__ __forceinline__ void load_tile_scales(TileScales& t, const AttnArgs& a, int bh, int tile,
+                                                 int tid) {
+    const int N = a.N, nb = a.nb;
     if (tid < 128) {
+        const int gk = min(tile * 128 + tid, N - 1);
+        t.b[0] = *reinterpret_cast<const uint32_t*>(a.ks + ((int64_t)bh * N + gk) * 4);
+    } else {
+        const uint8_t* vs = a.vs + ((int64_t)bh * 128 + (tid - 128)) * nb;
+#pragma unroll
+        for (int kb = 0; kb < 4; kb++) t.b[kb] = vs[min(4 * tile + kb, nb - 1)];
+    }
+}
+
+__device__ __forceinline__ void store_tile_scales(uint8_t* st, const TileScales& t, int tid) {
+    if (tid < 128) {
+        // K^ scale of (key, d-block db) goes to lane r + 32*(db&1), byte
+        // 4c + 2j + (db>>1) (S product of chunk c, tile j, channel half db>>1)
         const int key = tid;
-        const int gk = min(k0 + key, N - 1);
-        const uint32_t s4 = *reinterpret_cast<const uint32_t*>(a.ks + (krow0 + gk) * 4);
         int j, r;
         key_slot(key & 63, j, r);
         const int c = key >> 6;
 #pragma unroll
-        for (int db = 0; db < 4; db++) {
-            const int lane = r + 32 * (db & 1);
-            lds[kKsOff + lane * 8 + c * 4 + j * 2 + (db >> 1)] = (uint8_t)(s4 >> (8 * db));
-        }
-    }
-    // V^ codes: 128 channel rows x 4 key blocks of 16 B (blocks past the end
-    // read the last block; the matching P^ entries are zero)
-    const int64_t vrow0 = (int64_t)bh * 128;
+        for (int db = 0; db < 4; db++)
+            st[kKsOff + (r + 32 * (db & 1)) * 8 + c * 4 + j * 2 + (db >> 1)] = (uint8_t)(t.b[0] >> (8 * db));
+    } else {
+        // V^ scale of (channel d, key block kb) goes to lane d%32 + 32*(kb&1),
+        // byte 2*(d/32) + (kb>>1) (PV product of channel tile d/32, chunk kb>>1)
+        const int d = tid - 128;
 #pragma unroll
-    for (int it = 0; it < 2; it++) {
-        const int idx = tid + kThreads * it;
-        const int d = idx >> 2, kb = idx & 3;
-        const int blk = min(4 * tile + kb, nb - 1);
-        const uint4 v =
-            *reinterpret_cast<const uint4*>(a.vc + ((vrow0 + d) * nb + blk) * 16);
-        *reinterpret_cast<uint4*>(lds + kVcOff + d * 64 + 16 * (kb ^ swz(d))) = v;
-    }
-    // V^ scales: lane (d%32 + 32*(kb&1)) of PV product (channel tile d/32,
-    // chunk kb>>1)
-    if (tid < 128) {
-        const int d = tid;
-#pragma unroll
-        for (int kb = 0; kb < 4; kb++) {
-            const int blk = min(4 * tile + kb, nb - 1);
-            const uint8_t s = a.vs[(vrow0 + d) * nb + blk];
-            const int lane = (d & 31) + 32 * (kb & 1);
-            lds[kVsOff + lane * 8 + (d >> 5) * 2 + (kb >> 1)] = s;
-        }
+        for (int kb = 0; kb < 4; kb++)
+            st[kVsOff + ((d & 31) + 32 * (kb & 1)) * 8 + (d >> 5) * 2 + (kb >> 1)] = (uint8_t)t.b[kb];
     }
 }
 
@@ -130,9 +157,18 @@ __device__ __forceinline__ v16f mfma_fp4(v8i a, v8i b, v16f c, int sa, int sb) {
     return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 4, 4, kScaleOpsel, sa, 0, sb);
 }
 
+__device__ __forceinline__ uint32_t cvt_fp4x2(uint32_t old, float a, float b, float scale, int sel) {
+    switch (sel) {
+        case 0: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, a, b, scale, 0);
+        case 1: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, a, b, scale, 1);
+        case 2: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, a, b, scale, 2);
+        default: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, a, b, scale, 3);
+    }
+}
+
 template <int kRule, bool kPnq>
 __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
-    __shared__ __attribute__((aligned(16))) uint8_t lds[kStageBytes];
+    __shared__ __attribute__((aligned(16))) uint8_t lds[2 * kStageBytes];
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
     const int q = lane & 31, h = lane >> 5;
@@ -149,6 +185,11 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
     const int64_t rowbase = (int64_t)bh * N;
     const int qi = qt * kQueryTile + wave * kQw + q;
     const int qic = min(qi, N - 1);
+    const int ntiles = (N + 127) / 128;
+
+    TileScales pf;
+    load_tile_codes(lds, a, bh, 0, wave, lane);
+    load_tile_scales(pf, a, bh, 0, tid);
 
     // Q^ as the B operand of S^T = K^ Q^T: lane (q, h) holds channel block
     // 2*hf + h of its query for the product over channels 64*hf..64*hf+63.
@@ -172,39 +213,64 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
 #pragma unroll
         for (int i = 0; i < 16; i++) O[n][i] = 0.f;
 
-    const int ntiles = (N + 127) / 128;
-    for (int tile = 0; tile < ntiles; tile++) {
-        __syncthreads();
-        stage_tile(lds, a, bh, tile, tid);
-        __syncthreads();
+    store_tile_scales(lds, pf, tid);
+    __builtin_amdgcn_s_waitcnt(0);  // direct LDS loads of tile 0 landed
+    __syncthreads();
 
-        const uint2 ksb = *reinterpret_cast<const uint2*>(lds + kKsOff + lane * 8);
-        const uint2 vsb = *reinterpret_cast<const uint2*>(lds + kVsOff + lane * 8);
+    for (int tile = 0; tile < ntiles; tile++) {
+        const uint8_t* st = lds + (tile & 1) * kStageBytes;
+        uint8_t* next = lds + ((tile + 1) & 1) * kStageBytes;
+        if (tile + 1 < ntiles) {
+            load_tile_codes(next, a, bh, tile + 1, wave, lane);
+            load_tile_scales(pf, a, bh, tile + 1, tid);
+        }
+
+        const uint2 ksb = *reinterpret_cast<const uint2*>(st + kKsOff + lane * 8);
+        const uint2 vsb = *reinterpret_cast<const uint2*>(st + kVsOff + lane * 8);
+
+        // ---- K^ operands for the 8 S products (chunk c, tile j, half hf)
+        v8i kop[2][2][2];
+#pragma unroll
+        for (int c = 0; c < 2; c++)
+#pragma unroll
+            for (int j = 0; j < 2; j++) {
+                const int row = 64 * c + 32 * j + q;
+                const uint8_t* rp = st + kKcOff + row * 64;
+                const int sw = swz(row);
+                kop[c][j][0] = fp4_operand(*reinterpret_cast<const uint4*>(rp + 16 * ((0 + h) ^ sw)));
+                kop[c][j][1] = fp4_operand(*reinterpret_cast<const uint4*>(rp + 16 * ((2 + h) ^ sw)));
+            }
 
         // ---- S^T = K^ Q^T: S[c][j][i] is key 64c + 32h + 16j + i of the tile
         v16f S[2][2];
 #pragma unroll
         for (int c = 0; c < 2; c++) {
+            const int sreg = c == 0 ? (int)ksb.x : (int)ksb.y;
 #pragma unroll
             for (int j = 0; j < 2; j++) {
-                const int row = 64 * c + 32 * j + q;
-                const uint8_t* rp = lds + kKcOff + row * 64;
-                const int sw = swz(row);
-                const v8i k0v = fp4_operand(*reinterpret_cast<const uint4*>(rp + 16 * ((0 + h) ^ sw)));
-                const v8i k1v = fp4_operand(*reinterpret_cast<const uint4*>(rp + 16 * ((2 + h) ^ sw)));
-                const int sreg = c == 0 ? (int)ksb.x : (int)ksb.y;
                 v16f acc;
 #pragma unroll
                 for (int i = 0; i < 16; i++) acc[i] = 0.f;
                 if (j == 0) {
-                    acc = mfma_fp4<0>(k0v, qB0, acc, sreg, qS0);
-                    acc = mfma_fp4<1>(k1v, qB1, acc, sreg, qS1);
+                    acc = mfma_fp4<0>(kop[c][j][0], qB0, acc, sreg, qS0);
+                    acc = mfma_fp4<1>(kop[c][j][1], qB1, acc, sreg, qS1);
                 } else {
-                    acc = mfma_fp4<2>(k0v, qB0, acc, sreg, qS0);
-                    acc = mfma_fp4<3>(k1v, qB1, acc, sreg, qS1);
+                    acc = mfma_fp4<2>(kop[c][j][0], qB0, acc, sreg, qS0);
+                    acc = mfma_fp4<3>(kop[c][j][1], qB1, acc, sreg, qS1);
                 }
                 S[c][j] = acc;
             }
+        }
+
+        // ---- V^ operands for the PV products (read now, used after softmax)
+        v8i vop[4][2];
+#pragma unroll
+        for (int n = 0; n < 4; n++) {
+            const int row = 32 * n + q;
+            const uint8_t* rp = st + kVcOff + row * 64;
+            const int sw = swz(row);
+            vop[n][0] = fp4_operand(*reinterpret_cast<const uint4*>(rp + 16 * ((0 + h) ^ sw)));
+            vop[n][1] = fp4_operand(*reinterpret_cast<const uint4*>(rp + 16 * ((2 + h) ^ sw)));
         }
 
         // ---- mask keys past the end of the sequence (last tile only)
@@ -257,13 +323,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
                 const float p1 =
                     __builtin_amdgcn_exp2f(__builtin_fmaf(S[c][(n + 1) >> 4][(n + 1) & 15], cl, -m_new));
                 if (!kPnq) lsum += p0 + p1;
-                const int wd = n >> 3;
-                switch ((n & 7) >> 1) {
-                    case 0: w[wd] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w[wd], p0, p1, sf, 0); break;
-                    case 1: w[wd] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w[wd], p0, p1, sf, 1); break;
-                    case 2: w[wd] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w[wd], p0, p1, sf, 2); break;
-                    default: w[wd] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w[wd], p0, p1, sf, 3); break;
-                }
+                w[n >> 3] = cvt_fp4x2(w[n >> 3], p0, p1, sf, (n & 7) >> 1);
             }
             P[c] = fp4_operand(make_uint4(w[0], w[1], w[2], w[3]));
         }
@@ -290,21 +350,20 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
         }
 #pragma unroll
         for (int n = 0; n < 4; n++) {
-            const int row = 32 * n + q;
-            const uint8_t* rp = lds + kVcOff + row * 64;
-            const int sw = swz(row);
-            const v8i v0 = fp4_operand(*reinterpret_cast<const uint4*>(rp + 16 * ((0 + h) ^ sw)));
-            const v8i v1 = fp4_operand(*reinterpret_cast<const uint4*>(rp + 16 * ((2 + h) ^ sw)));
             const int sreg = n < 2 ? (int)vsb.x : (int)vsb.y;
             // scale byte index 2n + c within the lane's 8 bytes
             if ((n & 1) == 0) {
-                O[n] = mfma_fp4<0>(v0, P[0], O[n], sreg, psc[0]);
-                O[n] = mfma_fp4<1>(v1, P[1], O[n], sreg, psc[1]);
+                O[n] = mfma_fp4<0>(vop[n][0], P[0], O[n], sreg, psc[0]);
+                O[n] = mfma_fp4<1>(vop[n][1], P[1], O[n], sreg, psc[1]);
             } else {
-                O[n] = mfma_fp4<2>(v0, P[0], O[n], sreg, psc[0]);
-                O[n] = mfma_fp4<3>(v1, P[1], O[n], sreg, psc[1]);
+                O[n] = mfma_fp4<2>(vop[n][0], P[0], O[n], sreg, psc[0]);
+                O[n] = mfma_fp4<3>(vop[n][1], P[1], O[n], sreg, psc[1]);
             }
         }
+
+        if (tile + 1 < ntiles) store_tile_scales(next, pf, tid);
+        __builtin_amdgcn_s_waitcnt(0);  // the next tile's direct LDS loads landed
+        __syncthreads();
     }
 
     // ---- O = O~ / l  -> bf16
