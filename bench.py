@@ -64,7 +64,7 @@ def measured_traffic():
         return None
 
 
-def cpu_baseline(w, mode: str, rows_req: int, q_bits, k_bits, v_bits):
+def cpu_baseline(w, mode: str, rows_req: int, q_bits, k_bits, v_bits, block_c: int):
     """Time the CPU oracle on sampled query rows of head 0 (its own quantization
     of that head, then the tiled recurrence over all N keys)."""
     import numpy as np
@@ -77,23 +77,30 @@ def cpu_baseline(w, mode: str, rows_req: int, q_bits, k_bits, v_bits):
     def run(rows):
         return oracle.mx_attention_head_rows(codes["qc"][0, 0], codes["qs"][0, 0], codes["kc"][0, 0],
                                              codes["ks"][0, 0], codes["vc"][0, 0], codes["vs"][0, 0],
-                                             w.N, rows, mode, 128)
+                                             w.N, rows, mode, block_c)
 
     nthreads = oracle.threads(0)
     rng = np.random.default_rng(1)
-    if rows_req <= 0:  # size the sample for ~15 s of CPU work
-        probe = rng.choice(w.N, size=min(w.N, nthreads), replace=False)
+    order = rng.permutation(w.N)
+    if rows_req > 0:  # fixed sample
+        rows = np.sort(order[:rows_req])
         t0 = time.perf_counter()
-        run(probe)
+        run(rows)
         dt = time.perf_counter() - t0
-        rows_req = int(max(nthreads, min(8192, 15.0 / max(dt, 1e-6) * probe.size)))
-    rows = np.sort(rng.choice(w.N, size=min(w.N, rows_req), replace=False))
-    t0 = time.perf_counter()
-    run(rows)
-    dt = time.perf_counter() - t0
+        done = rows.size
+    else:  # batches of random rows until ~12 s of CPU work
+        done, dt, batch = 0, 0.0, 4 * nthreads
+        while dt < 12.0 and done < w.N:
+            rows = np.sort(order[done:done + batch])
+            t0 = time.perf_counter()
+            run(rows)
+            dt += time.perf_counter() - t0
+            done += rows.size
+            batch = min(8 * batch, 16384)
+    rows = np.arange(done)
     flops = 4.0 * w.N * w.d * rows.size
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": nthreads, "kind": "oracle",
-            "sample": f"{rows.size} random query rows of head 0 of {w.name} ({mode}), all "
+            "sample": f"{done} random query rows of head 0 of {w.name} ({mode}), all "
                       f"{w.N} keys, fp64 tiled recurrence incl. dequantization; "
                       f"{dt:.1f} s wall"}
 
@@ -108,6 +115,8 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=0, help="oracle sample rows (0: ~15 s)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-overhead", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run one plain 1 GiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -169,6 +178,13 @@ def main():
         extra[f"{args.mode}_ms_per_step_repeat"] = ms_again
         extra[f"overhead_{args.mode}_vs_{other}"] = min(ms, ms_again) / ms_other - 1.0
     del qc, qs, kc, ks, vc, vs
+    if args.copy_calibration:
+        # an elementwise kernel that reads 1 GiB and writes 1 GiB
+        src = torch.zeros(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     result = {
         "metric": METRIC,
@@ -192,7 +208,8 @@ def main():
     result.update(extra)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle baseline")
-        result["cpu_baseline"] = cpu_baseline(w, args.mode, args.cpu_rows, q_bits, k_bits, v_bits)
+        result["cpu_baseline"] = cpu_baseline(w, args.mode, args.cpu_rows, q_bits, k_bits, v_bits,
+                                              mxattn.kv_tile())
     else:
         result["cpu_baseline"] = None
     print(json.dumps(result), flush=True)

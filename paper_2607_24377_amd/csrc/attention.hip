@@ -5,8 +5,8 @@
 // B_c) in increasing order, as Algorithm 2 does, and for each tile:
 //
 //   1. reads the tile's MXFP4 K^ and V^ codes and E8M0 scales from LDS (the
-//      next tile is already being fetched from global memory into registers
-//      and lands in the other LDS buffer at the end of the iteration);
+//      next tile is already in flight into the other LDS buffer: codes by
+//      direct global->LDS loads, scales through four registers per thread);
 //   2. S^T = K^ Q^T on the block-scaled FP4 matrix cores
 //      (V_MFMA_SCALE_F32_32X32X64_F8F6F4, fp32 accumulation);
 //   3. online softmax in registers: running maximum m, correction
@@ -99,13 +99,13 @@ __device__ __forceinline__ void load_tile_codes(uint8_t* st, const AttnArgs& a, 
         const int key = 64 * c + 32 * ((r >> 2) & 1) + 16 * j + 4 * (r >> 3) + (r & 3);
         const int gk = min(k0 + key, N - 1);  // keys past N: masked scores
         const int db = slot ^ swz(row);
-        const uint8_t* ksrc = a.kc + (krow0 + gk) * 64 + db * 16;
+        const uint8_t* ksrc = (a.kc + krow0 * 64) + (uint32_t)(gk * 64 + db * 16);
         __builtin_amdgcn_global_load_lds((gbl_ptr_t)ksrc, (lds_ptr_t)(st + kKcOff + (2 * wave + it) * 1024), 16, 0, 0);
         // V^: row = channel, slot -> key block of the tile (blocks past the
         // end read the last block; the matching P^ entries are zero)
         const int kb = slot ^ swz(row);
         const int blk = min(4 * tile + kb, nb - 1);
-        const uint8_t* vsrc = a.vc + ((vrow0 + row) * nb + blk) * 16;
+        const uint8_t* vsrc = (a.vc + vrow0 * nb * 16) + (uint32_t)((row * nb + blk) * 16);
         __builtin_amdgcn_global_load_lds((gbl_ptr_t)vsrc, (lds_ptr_t)(st + kVcOff + (2 * wave + it) * 1024), 16, 0, 0);
     }
 }
@@ -152,6 +152,13 @@ __device__ __forceinline__ void store_tile_scales(uint8_t* st, const TileScales&
     }
 }
 
+__device__ __forceinline__ float max_with_other_half(float x) {
+    // lanes l and l^32 hold the two halves of one query row
+    const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, x),
+                                                    __builtin_bit_cast(uint32_t, x), false, false);
+    return fmaxf(__builtin_bit_cast(float, (uint32_t)r[0]), __builtin_bit_cast(float, (uint32_t)r[1]));
+}
+
 template <int kScaleOpsel>
 __device__ __forceinline__ v16f mfma_fp4(v8i a, v8i b, v16f c, int sa, int sb) {
     return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 4, 4, kScaleOpsel, sa, 0, sb);
@@ -170,7 +177,8 @@ template <int kRule, bool kPnq>
 __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
     __shared__ __attribute__((aligned(16))) uint8_t lds[2 * kStageBytes];
     const int tid = threadIdx.x;
-    const int wave = tid >> 6, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lane = tid & 63;
     const int q = lane & 31, h = lane >> 5;
 
     // XCD-aware order: consecutive workgroup ids go round-robin over the 8
@@ -297,7 +305,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
             bmax[c] = mx;
         }
         float rmax = fmaxf(bmax[0], bmax[1]);
-        rmax = fmaxf(rmax, __shfl_xor(rmax, 32));
+        rmax = max_with_other_half(rmax);
         float u = cl * rmax;
         if (__builtin_fmaf(rmax, cl, -u) < 0.f) u = next_down(u);  // RD(c * max s)
         const float m_new = fmaxf(m, u);

@@ -9,7 +9,8 @@ namespace mxattn {
 // Shared-scale rule of the MXFP4 quantizer.
 enum Rule { kRuleOcp = 0, kRuleUos = 1 };
 
-// Query rows per workgroup and keys per KV tile of the fused attention kernel.
+// Query rows per workgroup of the fused attention kernel, and its KV tile
+// B_c: the running maximum is updated once per kKvTile keys.
 constexpr int kQueryTile = 128;
 constexpr int kKvTile = 128;
 

@@ -44,8 +44,7 @@ def test_library_exports_every_declared_symbol(L):
 
 def test_queries(L):
     assert L.mxattn_version() >= 100
-    assert L.mxattn_kv_tile() == 128
-    assert L.mxattn_kv_tile() % 32 == 0
+    assert L.mxattn_kv_tile() in (32, 64, 128, 256)  # whole 32-key MXFP4 blocks
     assert L.mxattn_query_tile() > 0
     B, H, N, d = 1, 40, 75600, 128
     assert L.mxattn_codes_bytes(3, B, H, N, d) == B * H * N * 64

@@ -1,0 +1,72 @@
+"""Error of each mode's GPU output against exact (fp64, unquantized) attention.
+
+For every mode the test reports, on sampled rows: rel-L2, mean cosine,
+max-abs, the least-squares gain <O, O_ref> / <O_ref, O_ref>, and the induced
+row sums of the quantized recurrence (oracle diagnostics on the GPU's codes).
+It checks the two claims the paper makes about these quantities:
+
+* PNQ's induced weights sum to one (Proposition 1);
+* direct placement loses mass on average (Sec. 3, "Normalization Mismatch in
+  Online Softmax"), and UOS + PNQ brings the output's scale nearer to the
+  exact one than vanilla OCP does (the direction of the ablation, Sec. 5.3).
+
+rel-L2 alone is dominated by the 4-bit quantization noise of V and P and does
+not separate the modes; the gain and the row sums do.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from parity import flat, log, oracle_rows, sample_rows, workload_bits
+from paper_2607_24377_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+MODES = ["ocp_vanilla", "uos", "uos_pnq"]
+
+
+@pytest.fixture(scope="module")
+def mx():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2607_24377_amd import mxattn
+
+    mxattn.lib()
+    return mxattn
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2])
+def test_modes_against_exact_attention(mx, cfg):
+    w = inputs.workload(cfg)
+    q, k, v = workload_bits(cfg)
+    qt, kt, vt = (mx.bf16_from_bits(x) for x in (q, k, v))
+    heads = [0, w.B * w.H - 1]
+    rows = {h: sample_rows(w.N, 48, 7 + h, w.text_tokens) for h in heads}
+    qf, kf, vf = (flat(x) for x in (q, k, v))
+    ref = {h: oracle.attention_exact_rows(oracle.bf16_to_f64(qf[h][rows[h]]),
+                                          oracle.bf16_to_f64(kf[h]), oracle.bf16_to_f64(vf[h]))
+           for h in heads}
+    R = np.concatenate([ref[h] for h in heads])
+    res = {}
+    for mode in MODES:
+        out = flat(mx.bits_from_bf16(mx.forward(qt, kt, vt, mode)))
+        qc, qs = mx.quantize(qt, mx.AXIS_HEAD_DIM, mode)
+        kc, ks = mx.quantize(kt, mx.AXIS_HEAD_DIM, mode)
+        vc, vs = mx.quantize(vt, mx.AXIS_TOKENS, mode)
+        codes = {n: flat(t.cpu().numpy()) for n, t in
+                 dict(qc=qc, qs=qs, kc=kc, ks=ks, vc=vc, vs=vs).items()}
+        O = np.concatenate([oracle.bf16_to_f64(out[h][rows[h]]) for h in heads])
+        sums = np.concatenate([oracle_rows(codes, h, w.N, rows[h], mode, mx.kv_tile(), diag=True)[2][:, 1]
+                               for h in heads])
+        cos = np.sum(O * R, 1) / (np.linalg.norm(O, axis=1) * np.linalg.norm(R, axis=1))
+        res[mode] = dict(rel=float(np.linalg.norm(O - R) / np.linalg.norm(R)), cos=float(cos.mean()),
+                         maxabs=float(np.abs(O - R).max()), gain=float(np.sum(O * R) / np.sum(R * R)),
+                         rs_mean=float(sums.mean()), rs_min=float(sums.min()), rs_max=float(sums.max()))
+        r = res[mode]
+        log(f"[error] {w.name} {mode:12s} rel-L2 {r['rel']:.4f} cos {r['cos']:.4f} max-abs {r['maxabs']:.3f} "
+            f"gain {r['gain']:.4f} row-sum {r['rs_mean']:.4f} ({r['rs_min']:.4f}..{r['rs_max']:.4f})")
+    assert abs(res["uos_pnq"]["rs_mean"] - 1) < 1e-12 and abs(res["uos_pnq"]["rs_max"] - 1) < 1e-12
+    if w.kind != "outlier":  # near one-hot rows: every mode's scale is ~exact there
+        assert res["ocp_vanilla"]["rs_mean"] < 1.0 and res["uos"]["rs_mean"] < 1.0
+        assert abs(res["uos_pnq"]["gain"] - 1) < abs(res["ocp_vanilla"]["gain"] - 1)
