@@ -159,6 +159,37 @@ __device__ __forceinline__ float max_with_other_half(float x) {
     return fmaxf(__builtin_bit_cast(float, (uint32_t)r[0]), __builtin_bit_cast(float, (uint32_t)r[1]));
 }
 
+// LDS reads issued as inline assembly.  The compiler does not see them as LDS
+// accesses, so it does not make them wait for the direct global->LDS loads
+// of the next tile (which it cannot tell apart from the stage being read);
+// completion is awaited explicitly with lds_wait().
+typedef int v4i __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+__device__ __forceinline__ v4i lds_read128(uint32_t addr) {
+    v4i r;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(addr));
+    return r;
+}
+__device__ __forceinline__ uint2 lds_read64(uint32_t addr) {
+    uint2 r;
+    asm volatile("ds_read_b64 %0, %1" : "=v"(r) : "v"(addr));
+    return r;
+}
+__device__ __forceinline__ v8i fp4_v(v4i x) {
+    v8i r;
+    r[0] = x[0];
+    r[1] = x[1];
+    r[2] = x[2];
+    r[3] = x[3];
+    r[4] = 0;
+    r[5] = 0;
+    r[6] = 0;
+    r[7] = 0;
+    return r;
+}
+
 template <int kScaleOpsel>
 __device__ __forceinline__ v16f mfma_fp4(v8i a, v8i b, v16f c, int sa, int sb) {
     return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 4, 4, kScaleOpsel, sa, 0, sb);
@@ -233,11 +264,11 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
             load_tile_scales(pf, a, bh, tile + 1, tid);
         }
 
-        const uint2 ksb = *reinterpret_cast<const uint2*>(st + kKsOff + lane * 8);
-        const uint2 vsb = *reinterpret_cast<const uint2*>(st + kVsOff + lane * 8);
+        uint2 ksb = lds_read64(lds_addr(st + kKsOff + lane * 8));
+        uint2 vsb = lds_read64(lds_addr(st + kVsOff + lane * 8));
 
         // ---- K^ operands for the 8 S products (chunk c, tile j, half hf)
-        v8i kop[2][2][2];
+        v4i kr[2][2][2];
 #pragma unroll
         for (int c = 0; c < 2; c++)
 #pragma unroll
@@ -245,8 +276,20 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
                 const int row = 64 * c + 32 * j + q;
                 const uint8_t* rp = st + kKcOff + row * 64;
                 const int sw = swz(row);
-                kop[c][j][0] = fp4_operand(*reinterpret_cast<const uint4*>(rp + 16 * ((0 + h) ^ sw)));
-                kop[c][j][1] = fp4_operand(*reinterpret_cast<const uint4*>(rp + 16 * ((2 + h) ^ sw)));
+                kr[c][j][0] = lds_read128(lds_addr(rp + 16 * ((0 + h) ^ sw)));
+                kr[c][j][1] = lds_read128(lds_addr(rp + 16 * ((2 + h) ^ sw)));
+            }
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(kr[0][0][0]), "+v"(kr[0][0][1]), "+v"(kr[0][1][0]), "+v"(kr[0][1][1]),
+                       "+v"(kr[1][0][0]), "+v"(kr[1][0][1]), "+v"(kr[1][1][0]), "+v"(kr[1][1][1]), "+v"(ksb),
+                       "+v"(vsb));
+        v8i kop[2][2][2];
+#pragma unroll
+        for (int c = 0; c < 2; c++)
+#pragma unroll
+            for (int j = 0; j < 2; j++) {
+                kop[c][j][0] = fp4_v(kr[c][j][0]);
+                kop[c][j][1] = fp4_v(kr[c][j][1]);
             }
 
         // ---- S^T = K^ Q^T: S[c][j][i] is key 64c + 32h + 16j + i of the tile
@@ -271,14 +314,14 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
         }
 
         // ---- V^ operands for the PV products (read now, used after softmax)
-        v8i vop[4][2];
+        v4i vr[4][2];
 #pragma unroll
         for (int n = 0; n < 4; n++) {
             const int row = 32 * n + q;
             const uint8_t* rp = st + kVcOff + row * 64;
             const int sw = swz(row);
-            vop[n][0] = fp4_operand(*reinterpret_cast<const uint4*>(rp + 16 * ((0 + h) ^ sw)));
-            vop[n][1] = fp4_operand(*reinterpret_cast<const uint4*>(rp + 16 * ((2 + h) ^ sw)));
+            vr[n][0] = lds_read128(lds_addr(rp + 16 * ((0 + h) ^ sw)));
+            vr[n][1] = lds_read128(lds_addr(rp + 16 * ((2 + h) ^ sw)));
         }
 
         // ---- mask keys past the end of the sequence (last tile only)
@@ -350,6 +393,15 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
         lacc = alpha * lacc + dl;
 
         // ---- O~^T = diag(alpha) O~^T + V^T P^T
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(vr[0][0]), "+v"(vr[0][1]), "+v"(vr[1][0]), "+v"(vr[1][1]), "+v"(vr[2][0]),
+                       "+v"(vr[2][1]), "+v"(vr[3][0]), "+v"(vr[3][1]));
+        v8i vop[4][2];
+#pragma unroll
+        for (int n = 0; n < 4; n++) {
+            vop[n][0] = fp4_v(vr[n][0]);
+            vop[n][1] = fp4_v(vr[n][1]);
+        }
         if (__any(alpha != 1.f)) {
 #pragma unroll
             for (int n = 0; n < 4; n++)
