@@ -114,9 +114,16 @@ int mxattn_quantize(const void* x, uint8_t* codes, uint8_t* scales, int block_ax
     return MXATTN_OK;
 }
 
+// Rearranges the K^/V^ scales into sc (mxattn::tile_scales_bytes(B*H, N)
+// bytes of workspace), then runs the fused attention kernel.
 static int launch_attend(const uint8_t* qc, const uint8_t* qs, const uint8_t* kc,
-                         const uint8_t* ks, const uint8_t* vc, const uint8_t* vs, void* out,
-                         int64_t B, int64_t H, int64_t N, int mode, hipStream_t s) {
+                         const uint8_t* ks, const uint8_t* vc, const uint8_t* vs, uint8_t* sc,
+                         void* out, int64_t B, int64_t H, int64_t N, int mode, hipStream_t s) {
+    hipError_t e = mxattn::launch_tile_scales(ks, vs, sc, B * H, N, s);
+    if (e != hipSuccess) {
+        set_error("scale layout launch", e);
+        return MXATTN_ERR_HIP;
+    }
     mxattn::AttnArgs a;
     a.qc = qc;
     a.qs = qs;
@@ -124,6 +131,7 @@ static int launch_attend(const uint8_t* qc, const uint8_t* qs, const uint8_t* kc
     a.ks = ks;
     a.vc = vc;
     a.vs = vs;
+    a.sc = sc;
     a.out = static_cast<uint16_t*>(out);
     a.N = (int)N;
     a.nb = (int)((N + 31) / 32);
@@ -132,7 +140,7 @@ static int launch_attend(const uint8_t* qc, const uint8_t* qs, const uint8_t* kc
     if (total > (int64_t)1 << 30) return MXATTN_ERR_SHAPE;
     a.total_tiles = (int)total;
     a.per_xcd = (int)((total + 7) / 8);
-    hipError_t e = mxattn::launch_attention(a, mode, s);
+    e = mxattn::launch_attention(a, mode, s);
     if (e != hipSuccess) {
         set_error("attention launch", e);
         return MXATTN_ERR_HIP;
@@ -150,8 +158,22 @@ int mxattn_attend(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t
     if (!aligned(q_codes, 16) || !aligned(k_codes, 16) || !aligned(v_codes, 16) ||
         !aligned(out, 16) || !aligned(k_scales, 4))
         return MXATTN_ERR_ALIGN;
-    return launch_attend(q_codes, q_scales, k_codes, k_scales, v_codes, v_scales, out, B, H, N,
-                         mode, reinterpret_cast<hipStream_t>(stream));
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    keep_pool_memory();
+    void* ws = nullptr;
+    hipError_t e = hipMallocAsync(&ws, (size_t)mxattn::tile_scales_bytes(B * H, N), s);
+    if (e != hipSuccess || !ws) {
+        set_error("hipMallocAsync", e);
+        return MXATTN_ERR_OOM;
+    }
+    int st = launch_attend(q_codes, q_scales, k_codes, k_scales, v_codes, v_scales,
+                           static_cast<uint8_t*>(ws), out, B, H, N, mode, s);
+    e = hipFreeAsync(ws, s);
+    if (st == MXATTN_OK && e != hipSuccess) {
+        set_error("hipFreeAsync", e);
+        st = MXATTN_ERR_HIP;
+    }
+    return st;
 }
 
 int mxattn_forward(const void* q, const void* k, const void* v, void* out, int64_t B, int64_t H,
@@ -169,7 +191,8 @@ int mxattn_forward(const void* q, const void* k, const void* v, void* out, int64
     const size_t v_codes = mxattn_codes_bytes(MXATTN_AXIS_TOKENS, B, H, N, d);
     const size_t v_scales = mxattn_scales_bytes(MXATTN_AXIS_TOKENS, B, H, N, d);
     auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-    const size_t total = 2 * up(qk_codes) + 2 * up(qk_scales) + up(v_codes) + up(v_scales);
+    const size_t tiled = (size_t)mxattn::tile_scales_bytes(B * H, N);
+    const size_t total = 2 * up(qk_codes) + 2 * up(qk_scales) + up(v_codes) + up(v_scales) + up(tiled);
 
     void* ws = nullptr;
     hipError_t e = hipMallocAsync(&ws, total, s);
@@ -189,6 +212,8 @@ int mxattn_forward(const void* q, const void* k, const void* v, void* out, int64
     uint8_t* ks = p;
     p += up(qk_scales);
     uint8_t* vs = p;
+    p += up(v_scales);
+    uint8_t* sc = p;
 
     const int rule = rule_of(mode);
     int st = MXATTN_OK;
@@ -198,7 +223,7 @@ int mxattn_forward(const void* q, const void* k, const void* v, void* out, int64
         set_error("quantize launch", e);
         st = MXATTN_ERR_HIP;
     } else {
-        st = launch_attend(qc, qs, kc, ks, vc, vs, out, B, H, N, mode, s);
+        st = launch_attend(qc, qs, kc, ks, vc, vs, sc, out, B, H, N, mode, s);
     }
     e = hipFreeAsync(ws, s);
     if (st == MXATTN_OK && e != hipSuccess) {

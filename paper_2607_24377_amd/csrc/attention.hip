@@ -57,9 +57,9 @@ constexpr int kQw = 32;  // query rows per wave
 
 // LDS stage layout (bytes); two stages
 constexpr int kKcOff = 0;      // K^ codes: 128 rows x 64 B, rows in MFMA order
-constexpr int kKsOff = 8192;   // K^ scales: 64 lanes x 8 B, pre-permuted per lane
-constexpr int kVcOff = 8704;   // V^ codes: 128 rows (channels) x 64 B (128 keys)
-constexpr int kVsOff = 16896;  // V^ scales: 64 lanes x 8 B
+constexpr int kVcOff = 8192;   // V^ codes: 128 rows (channels) x 64 B (128 keys)
+constexpr int kKsOff = 16384;  // K^ scales: 64 lanes x 8 B, in MFMA operand order
+constexpr int kVsOff = 16896;  // V^ scales: 64 lanes x 8 B, in MFMA operand order
 constexpr int kStageBytes = 17408;
 
 // 16-byte slot swizzle of a 64-byte LDS row: any 16 consecutive rows read at
@@ -110,46 +110,14 @@ __device__ __forceinline__ void load_tile_codes(uint8_t* st, const AttnArgs& a, 
     }
 }
 
-// The tile's E8M0 scales in flight through registers: threads 0..127 hold
-// the 4 K^ scale bytes of key `tid`, threads 128..255 the 4 V^ scale bytes
-// of channel `tid - 128` (one byte per register, so no wait is needed until
-// they are written to LDS).
-struct TileScales {
-    uint32_t b[4];
-};
-
-__device__ __forceinline__ void load_tile_scales(TileScales& t, const AttnArgs& a, int bh, int tile,
-                                                 int tid) {
-    const int N = a.N, nb = a.nb;
-    if (tid < 128) {
-        const int gk = min(tile * 128 + tid, N - 1);
-        t.b[0] = *reinterpret_cast<const uint32_t*>(a.ks + ((int64_t)bh * N + gk) * 4);
-    } else {
-        const uint8_t* vs = a.vs + ((int64_t)bh * 128 + (tid - 128)) * nb;
-#pragma unroll
-        for (int kb = 0; kb < 4; kb++) t.b[kb] = vs[min(4 * tile + kb, nb - 1)];
-    }
-}
-
-__device__ __forceinline__ void store_tile_scales(uint8_t* st, const TileScales& t, int tid) {
-    if (tid < 128) {
-        // K^ scale of (key, d-block db) goes to lane r + 32*(db&1), byte
-        // 4c + 2j + (db>>1) (S product of chunk c, tile j, channel half db>>1)
-        const int key = tid;
-        int j, r;
-        key_slot(key & 63, j, r);
-        const int c = key >> 6;
-#pragma unroll
-        for (int db = 0; db < 4; db++)
-            st[kKsOff + (r + 32 * (db & 1)) * 8 + c * 4 + j * 2 + (db >> 1)] = (uint8_t)(t.b[0] >> (8 * db));
-    } else {
-        // V^ scale of (channel d, key block kb) goes to lane d%32 + 32*(kb&1),
-        // byte 2*(d/32) + (kb>>1) (PV product of channel tile d/32, chunk kb>>1)
-        const int d = tid - 128;
-#pragma unroll
-        for (int kb = 0; kb < 4; kb++)
-            st[kVsOff + ((d & 31) + 32 * (kb & 1)) * 8 + (d >> 5) * 2 + (kb >> 1)] = (uint8_t)t.b[kb];
-    }
+// The tile's K^ and V^ scales, already in the lanes' MFMA operand order (see
+// tile_scales_kernel): one 1 KiB direct load by wave 0 into [kKsOff, kStageBytes).
+__device__ __forceinline__ void load_tile_scales(uint8_t* st, const AttnArgs& a, int bh, int tile, int wave,
+                                                 int lane) {
+    if (wave != 0) return;
+    const int ntiles = (a.N + 127) / 128;
+    const uint8_t* src = a.sc + ((int64_t)bh * ntiles + tile) * 1024 + lane * 16;
+    __builtin_amdgcn_global_load_lds((gbl_ptr_t)src, (lds_ptr_t)(st + kKsOff), 16, 0, 0);
 }
 
 __device__ __forceinline__ float max_with_other_half(float x) {
@@ -226,9 +194,8 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
     const int qic = min(qi, N - 1);
     const int ntiles = (N + 127) / 128;
 
-    TileScales pf;
     load_tile_codes(lds, a, bh, 0, wave, lane);
-    load_tile_scales(pf, a, bh, 0, tid);
+    load_tile_scales(lds, a, bh, 0, wave, lane);
 
     // Q^ as the B operand of S^T = K^ Q^T: lane (q, h) holds channel block
     // 2*hf + h of its query for the product over channels 64*hf..64*hf+63.
@@ -252,7 +219,6 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
 #pragma unroll
         for (int i = 0; i < 16; i++) O[n][i] = 0.f;
 
-    store_tile_scales(lds, pf, tid);
     __builtin_amdgcn_s_waitcnt(0);  // direct LDS loads of tile 0 landed
     __syncthreads();
 
@@ -261,7 +227,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
         uint8_t* next = lds + ((tile + 1) & 1) * kStageBytes;
         if (tile + 1 < ntiles) {
             load_tile_codes(next, a, bh, tile + 1, wave, lane);
-            load_tile_scales(pf, a, bh, tile + 1, tid);
+            load_tile_scales(next, a, bh, tile + 1, wave, lane);
         }
 
         uint2 ksb = lds_read64(lds_addr(st + kKsOff + lane * 8));
@@ -421,7 +387,6 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
             }
         }
 
-        if (tile + 1 < ntiles) store_tile_scales(next, pf, tid);
         __builtin_amdgcn_s_waitcnt(0);  // the next tile's direct LDS loads landed
         __syncthreads();
     }
@@ -447,6 +412,55 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
 }
 
 }  // namespace
+
+// E8M0 scales of K^ ([BH, N, 4]) and V^ ([BH, 128, nb]) rearranged into the
+// order of the attention kernel's MFMA scale operands: per head and 128-key
+// tile, 512 bytes of K^ scales then 512 bytes of V^ scales, 8 bytes per lane.
+// K^: lane r + 32*(db&1), byte 4c + 2j + (db>>1) holds the scale of channel
+// block db of the key in A-row r of S product (chunk c, tile j).  V^: lane
+// (d&31) + 32*(kb&1), byte 2*(d>>5) + (kb>>1) holds the scale of channel d,
+// key block kb of the tile.  Keys past N repeat key N-1 and blocks past the
+// end repeat the last block, as the code loads do.
+__global__ __launch_bounds__(256) void tile_scales_kernel(const uint8_t* __restrict__ ks,
+                                                          const uint8_t* __restrict__ vs,
+                                                          uint8_t* __restrict__ out, int N, int nb,
+                                                          int ntiles, int64_t total) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;  // (head, tile, K|V, lane)
+    if (i >= total) return;
+    const int L = (int)(i & 63);
+    const int half = (int)((i >> 6) & 1);
+    const int64_t ht = i >> 7;
+    const int t = (int)(ht % ntiles);
+    const int64_t bh = ht / ntiles;
+    uint32_t lo = 0, hi = 0;
+#pragma unroll
+    for (int e = 0; e < 8; e++) {
+        uint32_t b;
+        if (half == 0) {
+            const int r = L & 31, c = e >> 2, j = (e >> 1) & 1, db = 2 * (e & 1) + (L >> 5);
+            const int w = (r & 3) | ((r >> 3) << 2) | (j << 4) | (((r >> 2) & 1) << 5);
+            const int key = min(t * 128 + 64 * c + w, N - 1);
+            b = ks[(bh * N + key) * 4 + db];
+        } else {
+            const int d = 32 * (e >> 1) + (L & 31), kb = 2 * (e & 1) + (L >> 5);
+            b = vs[(bh * 128 + d) * nb + min(4 * t + kb, nb - 1)];
+        }
+        if (e < 4)
+            lo |= b << (8 * e);
+        else
+            hi |= b << (8 * (e - 4));
+    }
+    *reinterpret_cast<uint2*>(out + ht * 1024 + half * 512 + L * 8) = make_uint2(lo, hi);
+}
+
+hipError_t launch_tile_scales(const uint8_t* ks, const uint8_t* vs, uint8_t* out, int64_t BH, int64_t N,
+                              hipStream_t stream) {
+    const int ntiles = (int)((N + 127) / 128);
+    const int64_t total = BH * ntiles * 128;
+    const dim3 grid((unsigned)((total + 255) / 256));
+    tile_scales_kernel<<<grid, 256, 0, stream>>>(ks, vs, out, (int)N, (int)((N + 31) / 32), ntiles, total);
+    return hipGetLastError();
+}
 
 hipError_t launch_attention(const AttnArgs& a, int mode, hipStream_t stream) {
     const dim3 grid((unsigned)(8 * a.per_xcd));

@@ -27,6 +27,7 @@ struct AttnArgs {
     const uint8_t* ks;  // [BH, N, 4]
     const uint8_t* vc;  // [BH, 128, nb * 16]
     const uint8_t* vs;  // [BH, 128, nb]
+    const uint8_t* sc;  // [BH, ntiles, 1024]: K^ and V^ scales in MFMA operand order
     uint16_t* out;      // [BH, N, 128] bf16
     int N;
     int nb;
@@ -34,6 +35,12 @@ struct AttnArgs {
     int total_tiles;
     int per_xcd;
 };
+
+// Scales of K^ and V^ in the attention kernel's operand order (AttnArgs::sc);
+// out holds tile_scales_bytes(BH, N) bytes.
+inline int64_t tile_scales_bytes(int64_t BH, int64_t N) { return BH * ((N + 127) / 128) * 1024; }
+hipError_t launch_tile_scales(const uint8_t* ks, const uint8_t* vs, uint8_t* out, int64_t BH, int64_t N,
+                              hipStream_t stream);
 
 // mode: 0 OCP + direct, 1 UOS + direct, 2 UOS + PNQ
 hipError_t launch_attention(const AttnArgs& a, int mode, hipStream_t stream);
