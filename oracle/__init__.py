@@ -32,7 +32,9 @@ MODES = {
     "ocp_vanilla": (RULE_OCP, 0),
     "uos": (RULE_UOS, 0),
     "uos_pnq": (RULE_UOS, 1),
+    "uos_pnq_rot": (RULE_UOS, 1),  # Q and K rotated by R_H before quantization
 }
+ROTATED = {"uos_pnq_rot"}
 
 _lock = threading.Lock()
 _lib = None
@@ -70,6 +72,10 @@ def lib() -> ctypes.CDLL:
             L.mxref_round_bf16.restype = None
             L.mxref_quantize_rows.argtypes = [P, I64, I64, I, P, P, I]
             L.mxref_quantize_rows.restype = I
+            L.mxref_quantize_rows_rotated.argtypes = [P, I64, I64, I, P, P, I]
+            L.mxref_quantize_rows_rotated.restype = I
+            L.mxref_hadamard_f32.argtypes = [P, I64]
+            L.mxref_hadamard_f32.restype = None
             L.mxref_quantize_keys.argtypes = [P, I64, I64, I64, I, P, P, I]
             L.mxref_quantize_keys.restype = I
             L.mxref_dequant_rows.argtypes = [P, P, I64, I64, P]
@@ -132,8 +138,9 @@ def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
 
 # ---------------------------------------------------------------- tensors
 
-def quantize_rows(x_bits: np.ndarray, rule: int, nthreads: int = 0):
-    """Blocks along the last axis.  x_bits: bf16 bits [..., d].
+def quantize_rows(x_bits: np.ndarray, rule: int, nthreads: int = 0, rotate: bool = False):
+    """Blocks along the last axis.  x_bits: bf16 bits [..., d].  With rotate,
+    each row is first multiplied by R_H (hadamard_f32, d = 128 only).
 
     Returns codes [..., d/2] and scales [..., d/32] (uint8)."""
     x = np.ascontiguousarray(x_bits, dtype=np.uint16)
@@ -141,10 +148,20 @@ def quantize_rows(x_bits: np.ndarray, rule: int, nthreads: int = 0):
     rows = x.size // d
     codes = np.empty(x.shape[:-1] + (d // 2,), dtype=np.uint8)
     scales = np.empty(x.shape[:-1] + (d // 32,), dtype=np.uint8)
-    rc = lib().mxref_quantize_rows(_ptr(x), rows, d, rule, _ptr(codes), _ptr(scales), nthreads)
+    fn = lib().mxref_quantize_rows_rotated if rotate else lib().mxref_quantize_rows
+    rc = fn(_ptr(x), rows, d, rule, _ptr(codes), _ptr(scales), nthreads)
     if rc != 0:
-        raise ValueError("mxref_quantize_rows rejected its arguments")
+        raise ValueError("oracle row quantizer rejected its arguments")
     return codes, scales
+
+
+def hadamard_f32(x: np.ndarray) -> np.ndarray:
+    """x R_H row by row (fp32 in, fp32 out), the oracle's fixed rotation."""
+    y = np.array(x, dtype=np.float32, order="C", copy=True)
+    d = y.shape[-1]
+    for row in y.reshape(-1, d):
+        lib().mxref_hadamard_f32(_ptr(row), d)
+    return y
 
 
 def quantize_keys(x_bits: np.ndarray, rule: int, nthreads: int = 0):
@@ -227,8 +244,9 @@ def quantize_qkv(q_bits, k_bits, v_bits, mode: str, nthreads: int = 0):
     Inputs are bf16 bits [B, H, N, d].  Returns a dict of codes/scales in the
     library's public layouts."""
     rule = MODES[mode][0]
-    qc, qs = quantize_rows(q_bits, rule, nthreads)
-    kc, ks = quantize_rows(k_bits, rule, nthreads)
+    rot = mode in ROTATED
+    qc, qs = quantize_rows(q_bits, rule, nthreads, rotate=rot)
+    kc, ks = quantize_rows(k_bits, rule, nthreads, rotate=rot)
     vc, vs = quantize_keys(v_bits, rule, nthreads)
     return dict(qc=qc, qs=qs, kc=kc, ks=ks, vc=vc, vs=vs)
 

@@ -259,6 +259,60 @@ int mxref_quantize_rows(const uint16_t* x, int64_t rows, int64_t d, int rule, ui
     return 0;
 }
 
+/* ------------------------------------------------------------------ */
+/* Fixed Hadamard rotation of Q and K (Sec. 3.3, Algorithm 2)          */
+/* ------------------------------------------------------------------ */
+
+/* x <- x R_H for one row of d = 2^k values, R_H = H / sqrt(d) with H the
+ * Sylvester Hadamard matrix, H[i][j] = (-1)^popcount(i & j) (symmetric, and
+ * orthogonal once scaled).  The paper fixes neither the size, the ordering
+ * nor the arithmetic; the reading here (shared with the GPU kernel's
+ * contract): natural Sylvester ordering without random signs, formed in fp32
+ * by the radix-2 fast Walsh-Hadamard transform with its stages in the order
+ * h = 1, 2, 4, ..., d/2, each stage mapping every pair (a, b) = (x[i], x[i+h])
+ * with bit h of i clear to (a + b, a - b), then one fp32 multiplication of
+ * each element by fp32(1/sqrt(d)). */
+void mxref_hadamard_f32(float* x, int64_t d) {
+    for (int64_t h = 1; h < d; h *= 2) {
+        for (int64_t i = 0; i < d; i++) {
+            if (i & h) continue;
+            float a = x[i], b = x[i + h];
+            x[i] = a + b;
+            x[i + h] = a - b;
+        }
+    }
+    const float s = (float)(1.0 / sqrt((double)d));
+    for (int64_t i = 0; i < d; i++) x[i] = x[i] * s;
+}
+
+/* Rows rotated by R_H, then quantized along the last axis as
+ * mxref_quantize_rows does (from the fp32 rotated values). */
+static void qrows_rot_range(void* p, int64_t r0, int64_t r1) {
+    qrows_ctx* c = (qrows_ctx*)p;
+    float y[128];
+    double v[32];
+    uint8_t cd[32];
+    for (int64_t r = r0; r < r1; r++) {
+        for (int64_t i = 0; i < c->d; i++) y[i] = (float)bf16_bits_to_double(c->x[r * c->d + i]);
+        mxref_hadamard_f32(y, c->d);
+        for (int64_t b = 0; b < c->d / 32; b++) {
+            for (int i = 0; i < 32; i++) v[i] = (double)y[b * 32 + i];
+            c->scales[r * (c->d / 32) + b] = quantize_block(v, 32, c->rule, cd);
+            uint8_t* dst = c->codes + r * (c->d / 2) + b * 16;
+            for (int i = 0; i < 16; i++) dst[i] = (uint8_t)(cd[2 * i] | (cd[2 * i + 1] << 4));
+        }
+    }
+}
+
+int mxref_quantize_rows_rotated(const uint16_t* x, int64_t rows, int64_t d, int rule, uint8_t* codes,
+                                uint8_t* scales, int nthreads) {
+    if (d != 128 || rows < 0) return -1;
+    if (rule != RULE_OCP && rule != RULE_UOS) return -1;
+    qrows_ctx c = {x, d, rule, codes, scales};
+    parallel_for(rows, nthreads, qrows_rot_range, &c);
+    return 0;
+}
+
 /* Blocks along the token axis: x is [heads, N, d] bf16.  For each (head,
  * channel) the N tokens form ceil(N/32) blocks of 32 consecutive tokens, the
  * last one padded with +0.  codes [heads, d, nb*16], scales [heads, d, nb]
