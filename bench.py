@@ -111,7 +111,7 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="video720p")
-    ap.add_argument("--mode", default="uos_pnq", choices=["ocp_vanilla", "uos", "uos_pnq"])
+    ap.add_argument("--mode", default="uos_pnq", choices=["ocp_vanilla", "uos", "uos_pnq", "uos_pnq_rot"])
     ap.add_argument("--cpu-rows", type=int, default=0, help="oracle sample rows (0: ~15 s)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-overhead", action="store_true")

@@ -50,8 +50,8 @@
 extern "C" {
 #endif
 
-/* Scale rule and row-sum placement (the rows of the paper's sequential
- * ablation, Sec. 5.3, without the Hadamard rotation):
+/* Scale rule, row-sum placement and rotation (rows of the paper's
+ * sequential ablation, Sec. 5.3):
  *   MXATTN_OCP_VANILLA  OCP floor rule for Q, K, V and P~; direct placement:
  *                       l accumulates the unquantized P~ (Eq.
  *                       direct_mxfp4_tile, Sec. 4.2).
@@ -59,11 +59,22 @@ extern "C" {
  *   MXATTN_UOS_PNQ      UOS rule everywhere; Pre-Normalization Quantization:
  *                       l accumulates the quantized P^ that also feeds the PV
  *                       product (Eqs. pnq_tile_contribution and
- *                       pnq_online_update; Algorithm 2). */
+ *                       pnq_online_update; Algorithm 2).
+ *   MXATTN_UOS_PNQ_ROT  as MXATTN_UOS_PNQ, and Q and K are multiplied by the
+ *                       fixed Hadamard rotation R_H = H/sqrt(128) before
+ *                       quantization (Sec. 3.3; Algorithm 2, its first two
+ *                       steps): Sylvester ordering, formed in fp32 by the
+ *                       radix-2 fast Walsh-Hadamard transform (stages
+ *                       h = 1, 2, ..., 64, pairs (a, b) -> (a + b, a - b)),
+ *                       then one fp32 multiply by fp32(1/sqrt(128)); the
+ *                       fp32 result is quantized directly.  V is not
+ *                       rotated.  Since (Q R_H)(K R_H)^T = Q K^T, the
+ *                       attention the operands represent is unchanged. */
 typedef enum {
     MXATTN_OCP_VANILLA = 0,
     MXATTN_UOS = 1,
-    MXATTN_UOS_PNQ = 2
+    MXATTN_UOS_PNQ = 2,
+    MXATTN_UOS_PNQ_ROT = 3
 } mxattn_mode;
 
 typedef enum {
@@ -82,7 +93,10 @@ typedef enum {
 #define MXATTN_AXIS_HEAD_DIM 3 /* blocks along d (Q and K) */
 
 /* MXFP4-quantize a bf16 tensor x [B, H, N, d] (Algorithm 1 with the scale
- * rule of `mode`: OCP floor for MXATTN_OCP_VANILLA, UOS otherwise).
+ * rule of `mode`: OCP floor for MXATTN_OCP_VANILLA, UOS otherwise).  With
+ * MXATTN_UOS_PNQ_ROT and block_axis MXATTN_AXIS_HEAD_DIM the rows are first
+ * rotated by R_H (Q and K of that mode); along MXATTN_AXIS_TOKENS that mode
+ * quantizes like MXATTN_UOS_PNQ.
  *   x       device, bf16 [B, H, N, d], 16-byte aligned
  *   codes   device, layout of `block_axis` above, 16-byte aligned,
  *           mxattn_codes_bytes() bytes
@@ -93,8 +107,8 @@ int mxattn_quantize(const void* x, uint8_t* codes, uint8_t* scales, int block_ax
                     int64_t B, int64_t H, int64_t N, int64_t d, void* stream);
 
 /* MXFP4 attention forward O = softmax(Q K^T / sqrt(d)) V with MXFP4 Q, K, V
- * and MXFP4 P~ (Algorithm 2 without rotation; non-causal, no mask besides
- * the sequence end).  Quantizes Q and K along d and V along N into
+ * and MXFP4 P~ (Algorithm 2, with its Hadamard rotation in mode
+ * MXATTN_UOS_PNQ_ROT only; non-causal, no mask besides the sequence end).  Quantizes Q and K along d and V along N into
  * stream-ordered workspace (hipMallocAsync/hipFreeAsync on `stream`, about
  * 0.53 bytes per element of each of Q, K, V), then runs the fused kernel.
  *   q, k, v  device bf16 [B, H, N, d], 16-byte aligned

@@ -25,7 +25,11 @@ void set_error(const char* what, hipError_t e) {
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
-bool valid_mode(int mode) { return mode >= MXATTN_OCP_VANILLA && mode <= MXATTN_UOS_PNQ; }
+bool valid_mode(int mode) { return mode >= MXATTN_OCP_VANILLA && mode <= MXATTN_UOS_PNQ_ROT; }
+
+// The attention kernel's mode: the rotated mode differs only in how Q and K
+// were quantized.
+int kernel_mode(int mode) { return mode == MXATTN_UOS_PNQ_ROT ? MXATTN_UOS_PNQ : mode; }
 
 // Shape limits of the kernels: 32-bit token indices, 64-bit byte offsets.
 int check_shape(int64_t B, int64_t H, int64_t N, int64_t d) {
@@ -69,7 +73,7 @@ const char* mxattn_status_string(int s) {
         case MXATTN_ERR_NULL: return "null pointer argument";
         case MXATTN_ERR_SHAPE: return "invalid shape (B, H, N must be >= 1 and within limits)";
         case MXATTN_ERR_ALIGN: return "misaligned pointer (tensors need 16-byte alignment)";
-        case MXATTN_ERR_MODE: return "invalid mode (0 ocp_vanilla, 1 uos, 2 uos_pnq)";
+        case MXATTN_ERR_MODE: return "invalid mode (0 ocp_vanilla, 1 uos, 2 uos_pnq, 3 uos_pnq_rot)";
         case MXATTN_ERR_AXIS: return "invalid block_axis (2 = tokens, 3 = head dim)";
         case MXATTN_ERR_UNSUPPORTED: return "unsupported head dimension (d must be 128)";
         case MXATTN_ERR_OOM: return "workspace allocation failed";
@@ -103,7 +107,9 @@ int mxattn_quantize(const void* x, uint8_t* codes, uint8_t* scales, int block_ax
     if (!aligned(x, 16) || !aligned(codes, 16)) return MXATTN_ERR_ALIGN;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     hipError_t e;
-    if (block_axis == MXATTN_AXIS_HEAD_DIM)
+    if (block_axis == MXATTN_AXIS_HEAD_DIM && mode == MXATTN_UOS_PNQ_ROT)
+        e = mxattn::launch_quantize_headdim_rotated(x, codes, scales, B * H * N, rule_of(mode), s);
+    else if (block_axis == MXATTN_AXIS_HEAD_DIM)
         e = mxattn::launch_quantize_headdim(x, codes, scales, B * H * N, rule_of(mode), s);
     else
         e = mxattn::launch_quantize_tokens(x, codes, scales, B * H, N, rule_of(mode), s);
@@ -140,7 +146,7 @@ static int launch_attend(const uint8_t* qc, const uint8_t* qs, const uint8_t* kc
     if (total > (int64_t)1 << 30) return MXATTN_ERR_SHAPE;
     a.total_tiles = (int)total;
     a.per_xcd = (int)((total + 7) / 8);
-    e = mxattn::launch_attention(a, mode, s);
+    e = mxattn::launch_attention(a, kernel_mode(mode), s);
     if (e != hipSuccess) {
         set_error("attention launch", e);
         return MXATTN_ERR_HIP;
@@ -217,8 +223,10 @@ int mxattn_forward(const void* q, const void* k, const void* v, void* out, int64
 
     const int rule = rule_of(mode);
     int st = MXATTN_OK;
-    if ((e = mxattn::launch_quantize_headdim(q, qc, qs, B * H * N, rule, s)) != hipSuccess ||
-        (e = mxattn::launch_quantize_headdim(k, kc, ks, B * H * N, rule, s)) != hipSuccess ||
+    auto qk = mode == MXATTN_UOS_PNQ_ROT ? mxattn::launch_quantize_headdim_rotated
+                                         : mxattn::launch_quantize_headdim;
+    if ((e = qk(q, qc, qs, B * H * N, rule, s)) != hipSuccess ||
+        (e = qk(k, kc, ks, B * H * N, rule, s)) != hipSuccess ||
         (e = mxattn::launch_quantize_tokens(v, vc, vs, B * H, N, rule, s)) != hipSuccess) {
         set_error("quantize launch", e);
         st = MXATTN_ERR_HIP;

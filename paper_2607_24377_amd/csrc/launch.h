@@ -17,6 +17,10 @@ constexpr int kKvTile = 128;
 hipError_t launch_quantize_headdim(const void* x, uint8_t* codes, uint8_t* scales, int64_t rows,
                                    int rule, hipStream_t stream);
 
+// Q/K of the rotated mode: rows multiplied by R_H = H/sqrt(128) first.
+hipError_t launch_quantize_headdim_rotated(const void* x, uint8_t* codes, uint8_t* scales, int64_t rows,
+                                           int rule, hipStream_t stream);
+
 hipError_t launch_quantize_tokens(const void* x, uint8_t* codes, uint8_t* scales, int64_t BH,
                                   int64_t N, int rule, hipStream_t stream);
 

@@ -56,6 +56,79 @@ __global__ __launch_bounds__(256) void quantize_headdim_kernel(const uint4* __re
 }
 
 // ---------------------------------------------------------------------------
+// Rotated head-dimension blocks (Q and K of the rotated mode): each row of 128
+// is multiplied by R_H = H/sqrt(128) (Sylvester Hadamard, Sec. 3.3, Algorithm
+// 2) before the block quantization above.  The product is the radix-2 fast
+// Walsh-Hadamard transform in fp32, stages h = 1, 2, 4, ..., 64, each mapping
+// (x[i], x[i+h]) (bit h of i clear) to (a + b, a - b), then one fp32 multiply
+// by fp32(1/sqrt(128)); the 16 threads of a row hold 8 consecutive elements
+// each, so stages 1-4 run in registers and stages 8-64 swap with the thread
+// whose row index differs in bit 0-3.  Every operation is a single correctly
+// rounded fp32 add, subtract or multiply in a fixed order, so the result is
+// bit-identical to any other evaluation in that order.
+// ---------------------------------------------------------------------------
+template <int kRule>
+__global__ __launch_bounds__(256) void quantize_headdim_rot_kernel(const uint4* __restrict__ x,
+                                                                   uint32_t* __restrict__ codes,
+                                                                   uint8_t* __restrict__ scales,
+                                                                   int64_t n_chunks) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const bool valid = i < n_chunks;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (valid) v = x[i];
+    const int t = threadIdx.x & 15;  // thread within the row: elements 8t..8t+7
+
+    float y[8];
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; e++) {
+        y[2 * e] = __builtin_bit_cast(float, w[e] << 16);
+        y[2 * e + 1] = __builtin_bit_cast(float, w[e] & 0xFFFF0000u);
+    }
+#pragma unroll
+    for (int h = 1; h < 8; h *= 2) {
+#pragma unroll
+        for (int e = 0; e < 8; e++) {
+            if (e & h) continue;
+            const float a = y[e], b = y[e + h];
+            y[e] = a + b;
+            y[e + h] = a - b;
+        }
+    }
+#pragma unroll
+    for (int m = 1; m < 16; m *= 2) {
+        const bool upper = (t & m) != 0;
+#pragma unroll
+        for (int e = 0; e < 8; e++) {
+            const float other = __shfl_xor(y[e], m);
+            y[e] = upper ? other - y[e] : y[e] + other;
+        }
+    }
+    const float rs = 0.0883883476483184405f;  // fp32(1/sqrt(128))
+#pragma unroll
+    for (int e = 0; e < 8; e++) y[e] = y[e] * rs;
+
+    // block maximum of |y| on the fp32 bit patterns
+    uint32_t m = 0;
+#pragma unroll
+    for (int e = 0; e < 8; e++) m = max(m, __builtin_bit_cast(uint32_t, y[e]) & 0x7FFFFFFFu);
+    m = max(m, (uint32_t)__shfl_xor((int)m, 1));
+    m = max(m, (uint32_t)__shfl_xor((int)m, 2));
+    const uint32_t sbyte = (m == 0) ? 127u : (uint32_t)(scale_exponent_f32<kRule>(m) + 127);
+    const float sf = e8m0_as_f32(sbyte);
+
+    uint32_t c = 0;
+    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[0], y[1], sf, 0);
+    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[2], y[3], sf, 1);
+    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[4], y[5], sf, 2);
+    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[6], y[7], sf, 3);
+    if (valid) {
+        codes[i] = c;
+        if ((i & 3) == 0) scales[i >> 2] = (uint8_t)sbyte;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Blocks along the token axis (V).  A workgroup stages 128 tokens x 128
 // channels of one head (32 KiB of bf16) in LDS with coalesced 16-byte loads;
 // wave w then quantizes token block w of the group, each lane owning a pair
@@ -148,6 +221,20 @@ hipError_t launch_quantize_headdim(const void* x, uint8_t* codes, uint8_t* scale
             (const uint4*)x, (uint32_t*)codes, scales, n_chunks);
     else
         quantize_headdim_kernel<kRuleOcp><<<grid, 256, 0, stream>>>(
+            (const uint4*)x, (uint32_t*)codes, scales, n_chunks);
+    return hipGetLastError();
+}
+
+hipError_t launch_quantize_headdim_rotated(const void* x, uint8_t* codes, uint8_t* scales, int64_t rows,
+                                           int rule, hipStream_t stream) {
+    const int64_t n_chunks = rows * 16;
+    if (n_chunks == 0) return hipSuccess;
+    const dim3 grid((unsigned)((n_chunks + 255) / 256));
+    if (rule == kRuleUos)
+        quantize_headdim_rot_kernel<kRuleUos><<<grid, 256, 0, stream>>>(
+            (const uint4*)x, (uint32_t*)codes, scales, n_chunks);
+    else
+        quantize_headdim_rot_kernel<kRuleOcp><<<grid, 256, 0, stream>>>(
             (const uint4*)x, (uint32_t*)codes, scales, n_chunks);
     return hipGetLastError();
 }

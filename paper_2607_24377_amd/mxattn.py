@@ -16,7 +16,7 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libmxattn.so")
 
-MODES = {"ocp_vanilla": 0, "uos": 1, "uos_pnq": 2}
+MODES = {"ocp_vanilla": 0, "uos": 1, "uos_pnq": 2, "uos_pnq_rot": 3}
 AXIS_TOKENS, AXIS_HEAD_DIM = 2, 3
 OK = 0
 

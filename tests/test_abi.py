@@ -67,7 +67,8 @@ def test_quantize_rejects_bad_arguments(L):
     assert q(None, FAKE, FAKE, 3, 2, 1, 1, 8, 128, None) == 1          # NULL
     assert q(FAKE, FAKE, None, 3, 2, 1, 1, 8, 128, None) == 1
     assert q(FAKE, FAKE, FAKE, 1, 2, 1, 1, 8, 128, None) == 5          # AXIS
-    assert q(FAKE, FAKE, FAKE, 3, 3, 1, 1, 8, 128, None) == 4          # MODE
+    assert q(FAKE, FAKE, FAKE, 3, 4, 1, 1, 8, 128, None) == 4          # MODE
+    assert q(FAKE, FAKE, FAKE, 3, 3, 0, 1, 8, 128, None) == 2          # mode 3 (rotated) is valid
     assert q(FAKE, FAKE, FAKE, 3, -1, 1, 1, 8, 128, None) == 4
     assert q(FAKE, FAKE, FAKE, 3, 2, 0, 1, 8, 128, None) == 2          # SHAPE
     assert q(FAKE, FAKE, FAKE, 2, 2, 1, 1, 0, 128, None) == 2

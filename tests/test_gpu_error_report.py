@@ -8,7 +8,9 @@ It checks the two claims the paper makes about these quantities:
 * PNQ's induced weights sum to one (Proposition 1);
 * direct placement loses mass on average (Sec. 3, "Normalization Mismatch in
   Online Softmax"), and UOS + PNQ brings the output's scale nearer to the
-  exact one than vanilla OCP does (the direction of the ablation, Sec. 5.3).
+  exact one than vanilla OCP does (the direction of the ablation, Sec. 5.3);
+* the Hadamard rotation of Q and K lowers the error where channels carry
+  outliers (its purpose in Sec. 3.3).
 
 rel-L2 alone is dominated by the 4-bit quantization noise of V and P and does
 not separate the modes; the gain and the row sums do.
@@ -23,7 +25,7 @@ from paper_2607_24377_amd import inputs
 pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
-MODES = ["ocp_vanilla", "uos", "uos_pnq"]
+MODES = ["ocp_vanilla", "uos", "uos_pnq", "uos_pnq_rot"]
 
 
 @pytest.fixture(scope="module")
@@ -66,7 +68,10 @@ def test_modes_against_exact_attention(mx, cfg):
         r = res[mode]
         log(f"[error] {w.name} {mode:12s} rel-L2 {r['rel']:.4f} cos {r['cos']:.4f} max-abs {r['maxabs']:.3f} "
             f"gain {r['gain']:.4f} row-sum {r['rs_mean']:.4f} ({r['rs_min']:.4f}..{r['rs_max']:.4f})")
-    assert abs(res["uos_pnq"]["rs_mean"] - 1) < 1e-12 and abs(res["uos_pnq"]["rs_max"] - 1) < 1e-12
+    for m in ("uos_pnq", "uos_pnq_rot"):
+        assert abs(res[m]["rs_mean"] - 1) < 1e-12 and abs(res[m]["rs_max"] - 1) < 1e-12
+    if w.kind == "outlier":
+        assert res["uos_pnq_rot"]["rel"] < res["uos_pnq"]["rel"]
     if w.kind != "outlier":  # near one-hot rows: every mode's scale is ~exact there
         assert res["ocp_vanilla"]["rs_mean"] < 1.0 and res["uos"]["rs_mean"] < 1.0
         assert abs(res["uos_pnq"]["gain"] - 1) < abs(res["ocp_vanilla"]["gain"] - 1)
