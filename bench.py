@@ -77,7 +77,7 @@ def cpu_baseline(w, mode: str, rows_req: int, q_bits, k_bits, v_bits, block_c: i
     def run(rows):
         return oracle.mx_attention_head_rows(codes["qc"][0, 0], codes["qs"][0, 0], codes["kc"][0, 0],
                                              codes["ks"][0, 0], codes["vc"][0, 0], codes["vs"][0, 0],
-                                             w.N, rows, mode, block_c)
+                                             w.n_kv, rows, mode, block_c)
 
     nthreads = oracle.threads(0)
     rng = np.random.default_rng(1)
@@ -98,10 +98,10 @@ def cpu_baseline(w, mode: str, rows_req: int, q_bits, k_bits, v_bits, block_c: i
             done += rows.size
             batch = min(8 * batch, 16384)
     rows = np.arange(done)
-    flops = 4.0 * w.N * w.d * rows.size
+    flops = 4.0 * w.n_kv * w.d * rows.size
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": nthreads, "kind": "oracle",
             "sample": f"{done} random query rows of head 0 of {w.name} ({mode}), all "
-                      f"{w.N} keys, fp64 tiled recurrence incl. dequantization; "
+                      f"{w.n_kv} keys, fp64 tiled recurrence incl. dequantization; "
                       f"{dt:.1f} s wall"}
 
 
@@ -141,7 +141,11 @@ def main():
     out = torch.empty_like(q)
     mxattn.lib()
 
+    cross = w.n_kv != w.N
+
     def fwd(mode):
+        if cross:
+            return lambda: mxattn.cross_forward(q, k, v, mode, out=out)
         return lambda: mxattn.forward(q, k, v, mode, out=out)
 
     log(f"[bench] timing forward {args.mode}: warmup {args.warmup}, steps {args.steps}")
@@ -153,7 +157,7 @@ def main():
     kc, ks = mxattn.quantize(k, mxattn.AXIS_HEAD_DIM, args.mode)
     vc, vs = mxattn.quantize(v, mxattn.AXIS_TOKENS, args.mode)
     log("[bench] timing the attention kernel alone")
-    attn_ms = time_ms(lambda: mxattn.attend(qc, qs, kc, ks, vc, vs, w.N, args.mode, out=out),
+    attn_ms = time_ms(lambda: mxattn.cross_attend(qc, qs, kc, ks, vc, vs, w.N, w.n_kv, args.mode, out=out),
                       args.steps, 1, torch)
     quant_ms = time_ms(lambda: mxattn.quantize(v, mxattn.AXIS_TOKENS, args.mode, codes=vc, scales=vs),
                        args.steps, 1, torch)
@@ -167,7 +171,7 @@ def main():
         "quantize_headdim_ms": quant_q_ms,
         "quantize_tokens_ms": quant_ms,
         "quantize_headdim_GBps": elems * 2.53125 / (quant_q_ms * 1e-3) / 1e9,
-        "quantize_tokens_GBps": elems * 2.53125 / (quant_ms * 1e-3) / 1e9,
+        "quantize_tokens_GBps": w.B * w.H * w.n_kv * w.d * 2.53125 / (quant_ms * 1e-3) / 1e9,
     }
     if not args.no_overhead:
         other = "ocp_vanilla" if args.mode != "ocp_vanilla" else "uos_pnq"
@@ -199,7 +203,7 @@ def main():
         "vs_baseline": None,
         "dtype": "mxfp4",
         "data": "synthetic",
-        "config": {"workload": w.name, "B": w.B, "H": w.H, "N": w.N, "d": w.d, "mode": args.mode,
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "N": w.N, "Nkv": w.n_kv, "d": w.d, "mode": args.mode,
                    "kv_tile": mxattn.kv_tile(), "query_tile": mxattn.query_tile()},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP4_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_FP4_TFLOPS,

@@ -128,6 +128,20 @@ int mxattn_attend(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t
                   const uint8_t* k_scales, const uint8_t* v_codes, const uint8_t* v_scales,
                   void* out, int64_t B, int64_t H, int64_t N, int64_t d, int mode, void* stream);
 
+/* Attention with different query and key/value lengths (cross-attention:
+ * video queries attending to a short text sequence; the paper's Wan2.2 has
+ * separate cross-attention modules, Sec. 5.1).  q and out are [B, H, Nq, d],
+ * k and v are [B, H, Nkv, d]; the quantized variants take Q^ blocked along d
+ * with Nq rows, K^ blocked along d with Nkv rows and V^ blocked along Nkv.
+ * Otherwise as mxattn_forward / mxattn_attend, which are these calls with
+ * Nq = Nkv = N. */
+int mxattn_cross_forward(const void* q, const void* k, const void* v, void* out, int64_t B,
+                         int64_t H, int64_t Nq, int64_t Nkv, int64_t d, int mode, void* stream);
+int mxattn_cross_attend(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
+                        const uint8_t* k_scales, const uint8_t* v_codes, const uint8_t* v_scales,
+                        void* out, int64_t B, int64_t H, int64_t Nq, int64_t Nkv, int64_t d, int mode,
+                        void* stream);
+
 /* Sizes of the code and scale arrays of a [B, H, N, d] tensor blocked along
  * `block_axis`; 0 for invalid arguments. */
 size_t mxattn_codes_bytes(int block_axis, int64_t B, int64_t H, int64_t N, int64_t d);

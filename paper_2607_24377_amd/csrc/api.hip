@@ -120,12 +120,13 @@ int mxattn_quantize(const void* x, uint8_t* codes, uint8_t* scales, int block_ax
     return MXATTN_OK;
 }
 
-// Rearranges the K^/V^ scales into sc (mxattn::tile_scales_bytes(B*H, N)
+// Rearranges the K^/V^ scales into sc (mxattn::tile_scales_bytes(B*H, Nkv)
 // bytes of workspace), then runs the fused attention kernel.
 static int launch_attend(const uint8_t* qc, const uint8_t* qs, const uint8_t* kc,
                          const uint8_t* ks, const uint8_t* vc, const uint8_t* vs, uint8_t* sc,
-                         void* out, int64_t B, int64_t H, int64_t N, int mode, hipStream_t s) {
-    hipError_t e = mxattn::launch_tile_scales(ks, vs, sc, B * H, N, s);
+                         void* out, int64_t B, int64_t H, int64_t Nq, int64_t Nkv, int mode,
+                         hipStream_t s) {
+    hipError_t e = mxattn::launch_tile_scales(ks, vs, sc, B * H, Nkv, s);
     if (e != hipSuccess) {
         set_error("scale layout launch", e);
         return MXATTN_ERR_HIP;
@@ -139,9 +140,10 @@ static int launch_attend(const uint8_t* qc, const uint8_t* qs, const uint8_t* kc
     a.vs = vs;
     a.sc = sc;
     a.out = static_cast<uint16_t*>(out);
-    a.N = (int)N;
-    a.nb = (int)((N + 31) / 32);
-    a.qtiles = (int)((N + mxattn::kQueryTile - 1) / mxattn::kQueryTile);
+    a.N = (int)Nkv;
+    a.Nq = (int)Nq;
+    a.nb = (int)((Nkv + 31) / 32);
+    a.qtiles = (int)((Nq + mxattn::kQueryTile - 1) / mxattn::kQueryTile);
     const int64_t total = B * H * a.qtiles;
     if (total > (int64_t)1 << 30) return MXATTN_ERR_SHAPE;
     a.total_tiles = (int)total;
@@ -154,26 +156,98 @@ static int launch_attend(const uint8_t* qc, const uint8_t* qs, const uint8_t* kc
     return MXATTN_OK;
 }
 
-int mxattn_attend(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
-                  const uint8_t* k_scales, const uint8_t* v_codes, const uint8_t* v_scales,
-                  void* out, int64_t B, int64_t H, int64_t N, int64_t d, int mode, void* stream) {
+int mxattn_cross_attend(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
+                        const uint8_t* k_scales, const uint8_t* v_codes, const uint8_t* v_scales,
+                        void* out, int64_t B, int64_t H, int64_t Nq, int64_t Nkv, int64_t d, int mode,
+                        void* stream) {
     if (!q_codes || !q_scales || !k_codes || !k_scales || !v_codes || !v_scales || !out)
         return MXATTN_ERR_NULL;
     if (!valid_mode(mode)) return MXATTN_ERR_MODE;
-    if (int st = check_shape(B, H, N, d)) return st;
+    if (int st = check_shape(B, H, Nq, d)) return st;
+    if (int st = check_shape(B, H, Nkv, d)) return st;
     if (!aligned(q_codes, 16) || !aligned(k_codes, 16) || !aligned(v_codes, 16) ||
         !aligned(out, 16) || !aligned(k_scales, 4))
         return MXATTN_ERR_ALIGN;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     keep_pool_memory();
     void* ws = nullptr;
-    hipError_t e = hipMallocAsync(&ws, (size_t)mxattn::tile_scales_bytes(B * H, N), s);
+    hipError_t e = hipMallocAsync(&ws, (size_t)mxattn::tile_scales_bytes(B * H, Nkv), s);
     if (e != hipSuccess || !ws) {
         set_error("hipMallocAsync", e);
         return MXATTN_ERR_OOM;
     }
     int st = launch_attend(q_codes, q_scales, k_codes, k_scales, v_codes, v_scales,
-                           static_cast<uint8_t*>(ws), out, B, H, N, mode, s);
+                           static_cast<uint8_t*>(ws), out, B, H, Nq, Nkv, mode, s);
+    e = hipFreeAsync(ws, s);
+    if (st == MXATTN_OK && e != hipSuccess) {
+        set_error("hipFreeAsync", e);
+        st = MXATTN_ERR_HIP;
+    }
+    return st;
+}
+
+int mxattn_attend(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
+                  const uint8_t* k_scales, const uint8_t* v_codes, const uint8_t* v_scales,
+                  void* out, int64_t B, int64_t H, int64_t N, int64_t d, int mode, void* stream) {
+    return mxattn_cross_attend(q_codes, q_scales, k_codes, k_scales, v_codes, v_scales, out, B, H, N,
+                               N, d, mode, stream);
+}
+
+int mxattn_cross_forward(const void* q, const void* k, const void* v, void* out, int64_t B,
+                         int64_t H, int64_t Nq, int64_t Nkv, int64_t d, int mode, void* stream) {
+    if (!q || !k || !v || !out) return MXATTN_ERR_NULL;
+    if (!valid_mode(mode)) return MXATTN_ERR_MODE;
+    if (int st = check_shape(B, H, Nq, d)) return st;
+    if (int st = check_shape(B, H, Nkv, d)) return st;
+    if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16))
+        return MXATTN_ERR_ALIGN;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    keep_pool_memory();
+
+    const size_t q_codes = mxattn_codes_bytes(MXATTN_AXIS_HEAD_DIM, B, H, Nq, d);
+    const size_t q_scales = mxattn_scales_bytes(MXATTN_AXIS_HEAD_DIM, B, H, Nq, d);
+    const size_t k_codes = mxattn_codes_bytes(MXATTN_AXIS_HEAD_DIM, B, H, Nkv, d);
+    const size_t k_scales = mxattn_scales_bytes(MXATTN_AXIS_HEAD_DIM, B, H, Nkv, d);
+    const size_t v_codes = mxattn_codes_bytes(MXATTN_AXIS_TOKENS, B, H, Nkv, d);
+    const size_t v_scales = mxattn_scales_bytes(MXATTN_AXIS_TOKENS, B, H, Nkv, d);
+    auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    const size_t tiled = (size_t)mxattn::tile_scales_bytes(B * H, Nkv);
+    const size_t total = up(q_codes) + up(k_codes) + up(v_codes) + up(q_scales) + up(k_scales) +
+                         up(v_scales) + up(tiled);
+
+    void* ws = nullptr;
+    hipError_t e = hipMallocAsync(&ws, total, s);
+    if (e != hipSuccess || !ws) {
+        set_error("hipMallocAsync", e);
+        return MXATTN_ERR_OOM;
+    }
+    uint8_t* p = static_cast<uint8_t*>(ws);
+    uint8_t* qc = p;
+    p += up(q_codes);
+    uint8_t* kc = p;
+    p += up(k_codes);
+    uint8_t* vc = p;
+    p += up(v_codes);
+    uint8_t* qs = p;
+    p += up(q_scales);
+    uint8_t* ks = p;
+    p += up(k_scales);
+    uint8_t* vs = p;
+    p += up(v_scales);
+    uint8_t* sc = p;
+
+    const int rule = rule_of(mode);
+    int st = MXATTN_OK;
+    auto qk = mode == MXATTN_UOS_PNQ_ROT ? mxattn::launch_quantize_headdim_rotated
+                                         : mxattn::launch_quantize_headdim;
+    if ((e = qk(q, qc, qs, B * H * Nq, rule, s)) != hipSuccess ||
+        (e = qk(k, kc, ks, B * H * Nkv, rule, s)) != hipSuccess ||
+        (e = mxattn::launch_quantize_tokens(v, vc, vs, B * H, Nkv, rule, s)) != hipSuccess) {
+        set_error("quantize launch", e);
+        st = MXATTN_ERR_HIP;
+    } else {
+        st = launch_attend(qc, qs, kc, ks, vc, vs, sc, out, B, H, Nq, Nkv, mode, s);
+    }
     e = hipFreeAsync(ws, s);
     if (st == MXATTN_OK && e != hipSuccess) {
         set_error("hipFreeAsync", e);
@@ -184,61 +258,7 @@ int mxattn_attend(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t
 
 int mxattn_forward(const void* q, const void* k, const void* v, void* out, int64_t B, int64_t H,
                    int64_t N, int64_t d, int mode, void* stream) {
-    if (!q || !k || !v || !out) return MXATTN_ERR_NULL;
-    if (!valid_mode(mode)) return MXATTN_ERR_MODE;
-    if (int st = check_shape(B, H, N, d)) return st;
-    if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16))
-        return MXATTN_ERR_ALIGN;
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    keep_pool_memory();
-
-    const size_t qk_codes = mxattn_codes_bytes(MXATTN_AXIS_HEAD_DIM, B, H, N, d);
-    const size_t qk_scales = mxattn_scales_bytes(MXATTN_AXIS_HEAD_DIM, B, H, N, d);
-    const size_t v_codes = mxattn_codes_bytes(MXATTN_AXIS_TOKENS, B, H, N, d);
-    const size_t v_scales = mxattn_scales_bytes(MXATTN_AXIS_TOKENS, B, H, N, d);
-    auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
-    const size_t tiled = (size_t)mxattn::tile_scales_bytes(B * H, N);
-    const size_t total = 2 * up(qk_codes) + 2 * up(qk_scales) + up(v_codes) + up(v_scales) + up(tiled);
-
-    void* ws = nullptr;
-    hipError_t e = hipMallocAsync(&ws, total, s);
-    if (e != hipSuccess || !ws) {
-        set_error("hipMallocAsync", e);
-        return MXATTN_ERR_OOM;
-    }
-    uint8_t* p = static_cast<uint8_t*>(ws);
-    uint8_t* qc = p;
-    p += up(qk_codes);
-    uint8_t* kc = p;
-    p += up(qk_codes);
-    uint8_t* vc = p;
-    p += up(v_codes);
-    uint8_t* qs = p;
-    p += up(qk_scales);
-    uint8_t* ks = p;
-    p += up(qk_scales);
-    uint8_t* vs = p;
-    p += up(v_scales);
-    uint8_t* sc = p;
-
-    const int rule = rule_of(mode);
-    int st = MXATTN_OK;
-    auto qk = mode == MXATTN_UOS_PNQ_ROT ? mxattn::launch_quantize_headdim_rotated
-                                         : mxattn::launch_quantize_headdim;
-    if ((e = qk(q, qc, qs, B * H * N, rule, s)) != hipSuccess ||
-        (e = qk(k, kc, ks, B * H * N, rule, s)) != hipSuccess ||
-        (e = mxattn::launch_quantize_tokens(v, vc, vs, B * H, N, rule, s)) != hipSuccess) {
-        set_error("quantize launch", e);
-        st = MXATTN_ERR_HIP;
-    } else {
-        st = launch_attend(qc, qs, kc, ks, vc, vs, sc, out, B, H, N, mode, s);
-    }
-    e = hipFreeAsync(ws, s);
-    if (st == MXATTN_OK && e != hipSuccess) {
-        set_error("hipFreeAsync", e);
-        st = MXATTN_ERR_HIP;
-    }
-    return st;
+    return mxattn_cross_forward(q, k, v, out, B, H, N, N, d, mode, stream);
 }
 
 }  // extern "C"

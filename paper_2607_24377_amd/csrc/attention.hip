@@ -188,10 +188,11 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
     if (logical >= a.total_tiles) return;
     const int bh = logical / a.qtiles;
     const int qt = logical - bh * a.qtiles;
-    const int N = a.N;
-    const int64_t rowbase = (int64_t)bh * N;
+    const int N = a.N;    // keys (and values)
+    const int Nq = a.Nq;  // queries (= N for self-attention)
+    const int64_t rowbase = (int64_t)bh * Nq;  // Q^ and O rows of this head
     const int qi = qt * kQueryTile + wave * kQw + q;
-    const int qic = min(qi, N - 1);
+    const int qic = min(qi, Nq - 1);
     const int ntiles = (N + 127) / 128;
 
     load_tile_codes(lds, a, bh, 0, wave, lane);
@@ -394,7 +395,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
     // ---- O = O~ / l  -> bf16
     float ltot = lacc;
     if (!kPnq) ltot += __shfl_xor(lacc, 32);
-    if (qi < N) {
+    if (qi < Nq) {
         uint16_t* orow = a.out + (int64_t)(rowbase + qi) * 128;
 #pragma unroll
         for (int n = 0; n < 4; n++) {

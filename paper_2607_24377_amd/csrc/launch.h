@@ -25,15 +25,16 @@ hipError_t launch_quantize_tokens(const void* x, uint8_t* codes, uint8_t* scales
                                   int64_t N, int rule, hipStream_t stream);
 
 struct AttnArgs {
-    const uint8_t* qc;  // [BH, N, 64]
-    const uint8_t* qs;  // [BH, N, 4]
+    const uint8_t* qc;  // [BH, Nq, 64]
+    const uint8_t* qs;  // [BH, Nq, 4]
     const uint8_t* kc;  // [BH, N, 64]
     const uint8_t* ks;  // [BH, N, 4]
     const uint8_t* vc;  // [BH, 128, nb * 16]
     const uint8_t* vs;  // [BH, 128, nb]
     const uint8_t* sc;  // [BH, ntiles, 1024]: K^ and V^ scales in MFMA operand order
-    uint16_t* out;      // [BH, N, 128] bf16
-    int N;
+    uint16_t* out;      // [BH, Nq, 128] bf16
+    int N;              // keys / values per head
+    int Nq;             // queries per head (Q^ codes/scales and out are [BH, Nq, ...])
     int nb;
     int qtiles;
     int total_tiles;

@@ -22,6 +22,13 @@ those settings imply stand in for them:
                           ``video480p``; text-token Q and K (after the offset)
                           scaled x4; V never scaled.
 
+Cross-attention (separate query and key/value lengths, as in Wan2.2's
+cross-attention modules, Sec. 5.1): ``cross720p`` has B=1 H=40, 75600 video
+queries distributed as ``video480p``'s Q, and 512 keys/values standing in
+for the text context (K Student-t df=4 scaled x2 with a per-(head, channel)
+offset drawn from N(0, variance 2), V N(0,1)); ``cross_ragged`` is a small
+case with ragged lengths.
+
 All configs use d=128 and bf16 storage (round to nearest even from fp32
 draws).  Every (tensor, head) pair has its own seed stream,
 ``SeedSequence(20260000 + config_index, spawn_key=(tensor, head))``, so any
@@ -48,11 +55,16 @@ class Workload:
     d: int
     kind: str
     text_tokens: int = 0
+    Nkv: int = 0  # keys/values per head if different from N (cross-attention)
+
+    @property
+    def n_kv(self) -> int:
+        return self.Nkv or self.N
 
     @property
     def flops(self) -> float:
-        """Algorithmic MXFP4 MFMA work of one forward: 4 * B * H * N^2 * d."""
-        return 4.0 * self.B * self.H * self.N * self.N * self.d
+        """Algorithmic MXFP4 MFMA work of one forward: 4 * B * H * N * Nkv * d."""
+        return 4.0 * self.B * self.H * self.N * self.n_kv * self.d
 
 
 WORKLOADS = [
@@ -62,7 +74,11 @@ WORKLOADS = [
     Workload(3, "video720p", 1, 40, 75600, 128, "video"),
     Workload(4, "joint_text_video", 1, 24, 119056, 128, "video", text_tokens=256),
 ]
-BY_NAME = {w.name: w for w in WORKLOADS}
+CROSS_WORKLOADS = [
+    Workload(10, "cross720p", 1, 40, 75600, 128, "cross", Nkv=512),
+    Workload(11, "cross_ragged", 1, 4, 1000, 128, "cross", Nkv=333),
+]
+BY_NAME = {w.name: w for w in WORKLOADS + CROSS_WORKLOADS}
 
 
 def workload(key) -> Workload:
@@ -103,10 +119,17 @@ def _student_t4(rng: np.random.Generator, shape) -> np.ndarray:
 
 
 def _head(w: Workload, b: int, h: int):
-    """fp32 Q, K, V [N, d] of one (batch, head)."""
+    """fp32 Q [N, d] and K, V [Nkv, d] of one (batch, head)."""
     head = b * w.H + h
     N, d = w.N, w.d
     rq, rk, rv, ra = (_rng(w, t, head) for t in (_Q, _K, _V, _AUX))
+    if w.kind == "cross":
+        q = _student_t4(rq, (N, d))
+        k = _student_t4(rk, (w.n_kv, d)) * np.float32(2.0)
+        mu = ra.normal(0.0, np.sqrt(2.0), size=d).astype(np.float32)
+        k += mu[None, :]
+        v = rv.standard_normal((w.n_kv, d), dtype=np.float32)
+        return q, k, v
     v = rv.standard_normal((N, d), dtype=np.float32)
     if w.kind == "iid":
         q = rq.standard_normal((N, d), dtype=np.float32)
@@ -138,9 +161,10 @@ def generate(key, heads=None, threads: int | None = None):
     all_heads = list(range(w.B * w.H))
     sel = all_heads if heads is None else list(heads)
     shape = (len(sel), w.N, w.d)
+    kv_shape = (len(sel), w.n_kv, w.d)
     Q = np.empty(shape, dtype=np.uint16)
-    K = np.empty(shape, dtype=np.uint16)
-    V = np.empty(shape, dtype=np.uint16)
+    K = np.empty(kv_shape, dtype=np.uint16)
+    V = np.empty(kv_shape, dtype=np.uint16)
 
     def one(i):
         b, h = divmod(sel[i], w.H)
@@ -157,6 +181,6 @@ def generate(key, heads=None, threads: int | None = None):
         with _cf.ThreadPoolExecutor(nt) as ex:
             list(ex.map(one, range(len(sel))))
     if heads is None:
-        out_shape = (w.B, w.H, w.N, w.d)
-        return Q.reshape(out_shape), K.reshape(out_shape), V.reshape(out_shape)
+        return (Q.reshape(w.B, w.H, w.N, w.d), K.reshape(w.B, w.H, w.n_kv, w.d),
+                V.reshape(w.B, w.H, w.n_kv, w.d))
     return Q, K, V

@@ -48,6 +48,10 @@ def lib() -> ctypes.CDLL:
             L.mxattn_forward.argtypes = [P, P, P, P, I64, I64, I64, I64, I, P]
             L.mxattn_forward.restype = I
             L.mxattn_attend.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I, P]
+            L.mxattn_cross_forward.argtypes = [P, P, P, P, I64, I64, I64, I64, I64, I, P]
+            L.mxattn_cross_forward.restype = I
+            L.mxattn_cross_attend.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I64, I, P]
+            L.mxattn_cross_attend.restype = I
             L.mxattn_attend.restype = I
             L.mxattn_codes_bytes.argtypes = [I, I64, I64, I64, I64]
             L.mxattn_codes_bytes.restype = SZ
@@ -143,6 +147,33 @@ def attend(qc, qs, kc, ks, vc, vs, N: int, mode, out=None, stream=None):
                              vc.data_ptr(), vs.data_ptr(), out.data_ptr(), B, H, N, d, _mode(mode),
                              _stream(stream))
     _check(st, "mxattn_attend")
+    return out
+
+
+def cross_forward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, mode, out=None, stream=None):
+    """Attention of bf16 q [B, H, Nq, d] over k, v [B, H, Nkv, d]; returns bf16 out [B, H, Nq, d]."""
+    B, H, Nq, d = _bhnd(q)
+    Bk, Hk, Nkv, dk = _bhnd(k)
+    if (Bk, Hk, dk) != (B, H, d) or _bhnd(v) != k.shape:
+        raise ValueError("k and v must be [B, H, Nkv, d] with q's B, H, d")
+    if out is None:
+        out = torch.empty_like(q)
+    st = lib().mxattn_cross_forward(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), B, H,
+                                    Nq, Nkv, d, _mode(mode), _stream(stream))
+    _check(st, "mxattn_cross_forward")
+    return out
+
+
+def cross_attend(qc, qs, kc, ks, vc, vs, Nq: int, Nkv: int, mode, out=None, stream=None):
+    """The fused kernel on quantized operands with Nq queries and Nkv keys."""
+    B, H = qc.shape[0], qc.shape[1]
+    d = qc.shape[3] * 2
+    if out is None:
+        out = torch.empty((B, H, Nq, d), dtype=torch.bfloat16, device=qc.device)
+    st = lib().mxattn_cross_attend(qc.data_ptr(), qs.data_ptr(), kc.data_ptr(), ks.data_ptr(),
+                                   vc.data_ptr(), vs.data_ptr(), out.data_ptr(), B, H, Nq, Nkv, d,
+                                   _mode(mode), _stream(stream))
+    _check(st, "mxattn_cross_attend")
     return out
 
 

@@ -87,6 +87,14 @@ def test_forward_and_attend_reject_bad_arguments(L):
     assert f(FAKE, FAKE, FAKE, FAKE, 1, 1, -5, 128, 2, None) == 2
     assert f(FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 256, 2, None) == 6
     assert f(FAKE, FAKE, FAKE + 4, FAKE, 1, 1, 8, 128, 2, None) == 3
+    c = L.mxattn_cross_forward
+    assert c(FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 0, 128, 2, None) == 2    # Nkv < 1
+    assert c(FAKE, FAKE, FAKE, FAKE, 1, 1, 0, 8, 128, 2, None) == 2    # Nq < 1
+    assert c(FAKE, None, FAKE, FAKE, 1, 1, 8, 8, 128, 2, None) == 1
+    assert c(FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 8, 128, 5, None) == 4
+    ca = L.mxattn_cross_attend
+    assert ca(*([FAKE] * 7), 1, 1, 8, 1 << 29, 128, 2, None) == 2
+    assert ca(*([FAKE] * 7), 1, 1, 8, 8, 64, 2, None) == 6
     a = L.mxattn_attend
     args = [FAKE] * 7
     bad = list(args)
