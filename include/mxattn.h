@@ -51,7 +51,7 @@ extern "C" {
 #endif
 
 /* Scale rule, row-sum placement and rotation (rows of the paper's
- * sequential ablation, Sec. 5.3):
+ * sequential ablation, Sec. 5.4):
  *   MXATTN_OCP_VANILLA  OCP floor rule for Q, K, V and P~; direct placement:
  *                       l accumulates the unquantized P~ (Eq.
  *                       direct_mxfp4_tile, Sec. 4.2).
@@ -62,7 +62,7 @@ extern "C" {
  *                       pnq_online_update; Algorithm 2).
  *   MXATTN_UOS_PNQ_ROT  as MXATTN_UOS_PNQ, and Q and K are multiplied by the
  *                       fixed Hadamard rotation R_H = H/sqrt(128) before
- *                       quantization (Sec. 3.3; Algorithm 2, its first two
+ *                       quantization (Sec. 4.3; Algorithm 2, its first two
  *                       steps): Sylvester ordering, formed in fp32 by the
  *                       radix-2 fast Walsh-Hadamard transform (stages
  *                       h = 1, 2, ..., 64, pairs (a, b) -> (a + b, a - b)),

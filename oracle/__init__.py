@@ -13,6 +13,9 @@ without the Hadamard rotation):
 * ``uos``: UOS rule (Algorithm 1) everywhere, direct placement.
 * ``uos_pnq``: UOS rule everywhere, Pre-Normalization Quantization
   (l accumulates the quantized P^; Eq. pnq_online_update, Algorithm 2).
+
+``objective`` holds the data-free objective J(q) of Sec. 4.1 (E(x), D(x),
+Delta(q)) used to check the boundary sweep.
 """
 from __future__ import annotations
 
@@ -74,6 +77,12 @@ def lib() -> ctypes.CDLL:
             L.mxref_quantize_rows.restype = I
             L.mxref_quantize_rows_rotated.argtypes = [P, I64, I64, I, P, P, I]
             L.mxref_quantize_rows_rotated.restype = I
+            L.mxref_quantize_block_qmax.argtypes = [P, I, ctypes.c_double, P, P]
+            L.mxref_quantize_block_qmax.restype = I
+            L.mxref_quantize_rows_qmax.argtypes = [P, I64, I64, ctypes.c_double, P, P]
+            L.mxref_quantize_rows_qmax.restype = I
+            L.mxref_qmax_sse.argtypes = [P, I64, I64, I64, I, P, I, P, I]
+            L.mxref_qmax_sse.restype = I
             L.mxref_hadamard_f32.argtypes = [P, I64]
             L.mxref_hadamard_f32.restype = None
             L.mxref_quantize_keys.argtypes = [P, I64, I64, I64, I, P, P, I]
@@ -153,6 +162,43 @@ def quantize_rows(x_bits: np.ndarray, rule: int, nthreads: int = 0, rotate: bool
     if rc != 0:
         raise ValueError("oracle row quantizer rejected its arguments")
     return codes, scales
+
+
+def quantize_block_qmax(values, q: float):
+    """Quantize up to 32 values with the ceil rule of boundary q (4 <= q <= 8)."""
+    v = np.ascontiguousarray(np.asarray(values, dtype=np.float64))
+    codes = np.zeros(v.size, dtype=np.uint8)
+    sc = np.zeros(1, dtype=np.uint8)
+    if lib().mxref_quantize_block_qmax(_ptr(v), v.size, float(q), _ptr(codes), _ptr(sc)) != 0:
+        raise ValueError("bad block or boundary")
+    return codes, int(sc[0])
+
+
+def quantize_rows_qmax(x_bits: np.ndarray, q: float):
+    """Blocks along the last axis with the ceil rule of boundary q."""
+    x = np.ascontiguousarray(x_bits, dtype=np.uint16)
+    d = x.shape[-1]
+    rows = x.size // d
+    codes = np.empty(x.shape[:-1] + (d // 2,), dtype=np.uint8)
+    scales = np.empty(x.shape[:-1] + (d // 32,), dtype=np.uint8)
+    if lib().mxref_quantize_rows_qmax(_ptr(x), rows, d, float(q), _ptr(codes), _ptr(scales)) != 0:
+        raise ValueError("bad arguments")
+    return codes, scales
+
+
+def qmax_sse(x_bits: np.ndarray, axis: int, qs, nthreads: int = 0) -> np.ndarray:
+    """Per-head sum of squared MXFP4 errors for each boundary in qs.
+
+    x_bits: bf16 bits [..., N, d]; axis 3 = blocks along d, 2 = along tokens.
+    Returns [heads, len(qs)] fp64."""
+    x = np.ascontiguousarray(x_bits, dtype=np.uint16)
+    N, d = x.shape[-2], x.shape[-1]
+    heads = x.size // (N * d)
+    q = np.ascontiguousarray(np.asarray(qs, dtype=np.float64))
+    out = np.empty((heads, q.size), dtype=np.float64)
+    if lib().mxref_qmax_sse(_ptr(x), heads, N, d, axis, _ptr(q), q.size, _ptr(out), nthreads) != 0:
+        raise ValueError("bad arguments")
+    return out
 
 
 def hadamard_f32(x: np.ndarray) -> np.ndarray:

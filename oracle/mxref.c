@@ -22,6 +22,11 @@
  *     OAS and the OCP Endpoint Convention" (Eq. app_ocp_floor).
  *   - UOS rule e = ceil(log2(M / 7.25)), all-zero block -> sigma = 1:
  *     Algorithm 1 (UOS-Based MXFP4 Block Quantization), Eq. uos_mapping.
+ *   - Generic ceil boundary q: e = ceil(log2(M / q)) (Eq. scale_definition,
+ *     Eq. uos_mapping) for 4 <= q <= 8, covering TFS (q = 6), OAS (q = 7,
+ *     App. "Relation to OAS and the OCP Endpoint Convention"), UOS (7.25) and
+ *     the ceil form of OCP (8); the per-head squared-error sweep over q of
+ *     the empirical check in Sec. 5.5 (Table cx_distribution).
  *   - Online softmax recurrence: Sec. 2 Eqs. online_attention /
  *     online_attention_output; direct placement: Eq. direct_mxfp4_tile;
  *     PNQ: Eqs. pnq_tile_contribution / pnq_online_update; Algorithm 2
@@ -260,7 +265,7 @@ int mxref_quantize_rows(const uint16_t* x, int64_t rows, int64_t d, int rule, ui
 }
 
 /* ------------------------------------------------------------------ */
-/* Fixed Hadamard rotation of Q and K (Sec. 3.3, Algorithm 2)          */
+/* Fixed Hadamard rotation of Q and K (Sec. 4.3, Algorithm 2)          */
 /* ------------------------------------------------------------------ */
 
 /* x <- x R_H for one row of d = 2^k values, R_H = H / sqrt(d) with H the
@@ -310,6 +315,119 @@ int mxref_quantize_rows_rotated(const uint16_t* x, int64_t rows, int64_t d, int 
     if (rule != RULE_OCP && rule != RULE_UOS) return -1;
     qrows_ctx c = {x, d, rule, codes, scales};
     parallel_for(rows, nthreads, qrows_rot_range, &c);
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* Generic boundary family q (Sec. 4.1, Theorem 1; App. "Relation to    */
+/* OAS and the OCP Endpoint Convention")                               */
+/* ------------------------------------------------------------------ */
+
+/* The ceil rule with boundary q: e = the smallest integer with M <= q 2^e
+ * (= ceil(log2(M/q))), clamped to [-127, 127]; q = 7.25 is UOS, q = 6 maps
+ * every block maximum into (3, 6] (no clipping), q = 8 is the ceil form of
+ * the OCP boundary.  Found by search, for 4 <= q <= 8. */
+static int scale_exponent_qmax(double M, double q) {
+    int e = ilogb(M) - 4; /* q 2^e <= 2^(ilogb(M)-1) < M: condition false */
+    while (!(M <= q * ldexp(1.0, e))) e++;
+    if (e < -127) e = -127;
+    if (e > 127) e = 127;
+    return e;
+}
+
+static uint8_t quantize_block_qmax(const double* v, int n, double q, uint8_t* out_codes) {
+    double M = 0.0;
+    for (int i = 0; i < n; i++)
+        if (fabs(v[i]) > M) M = fabs(v[i]);
+    if (M == 0.0) {
+        for (int i = 0; i < n; i++) out_codes[i] = (uint8_t)(signbit(v[i]) ? 8 : 0);
+        return 127;
+    }
+    int e = scale_exponent_qmax(M, q);
+    for (int i = 0; i < n; i++) {
+        int idx = nearest_grid_index(ldexp(fabs(v[i]), -e));
+        out_codes[i] = (uint8_t)((signbit(v[i]) ? 8 : 0) | idx);
+    }
+    return (uint8_t)(e + 127);
+}
+
+int mxref_quantize_block_qmax(const double* v, int n, double q, uint8_t* codes, uint8_t* scale) {
+    if (n < 1 || n > 32 || !(q >= 4.0 && q <= 8.0)) return -1;
+    *scale = quantize_block_qmax(v, n, q, codes);
+    return 0;
+}
+
+/* Blocks along the last axis with boundary q: x [rows, d] bf16 -> codes
+ * [rows, d/2], scales [rows, d/32], as mxref_quantize_rows. */
+int mxref_quantize_rows_qmax(const uint16_t* x, int64_t rows, int64_t d, double q, uint8_t* codes,
+                             uint8_t* scales) {
+    if (d <= 0 || d % 32 != 0 || rows < 0 || !(q >= 4.0 && q <= 8.0)) return -1;
+    double v[32];
+    uint8_t cd[32];
+    for (int64_t r = 0; r < rows; r++)
+        for (int64_t b = 0; b < d / 32; b++) {
+            for (int i = 0; i < 32; i++) v[i] = bf16_bits_to_double(x[r * d + b * 32 + i]);
+            scales[r * (d / 32) + b] = quantize_block_qmax(v, 32, q, cd);
+            for (int i = 0; i < 16; i++) codes[r * (d / 2) + b * 16 + i] = (uint8_t)(cd[2 * i] | (cd[2 * i + 1] << 4));
+        }
+    return 0;
+}
+
+/* Sum over a head's blocks of the squared quantization error sum_i (v_i -
+ * Q_q(v_i))^2, for each boundary in qs[0..nq): the per-tensor MSE sweep of
+ * the empirical check of Sec. 5.5 (Table cx_distribution).  axis 3: blocks
+ * along d of x [heads, N, d]; axis 2: blocks of 32 consecutive tokens per
+ * channel, the last one padded with +0 (padding adds no error).  sse is
+ * [heads, nq], fp64. */
+typedef struct {
+    const uint16_t* x;
+    int64_t N, d;
+    int axis;
+    const double* qs;
+    int nq;
+    double* sse;
+} sse_ctx;
+
+static void sse_range(void* p, int64_t h0, int64_t h1) {
+    sse_ctx* c = (sse_ctx*)p;
+    double v[32];
+    uint8_t cd[32];
+    const int64_t nb = (c->N + 31) / 32;
+    for (int64_t h = h0; h < h1; h++) {
+        const uint16_t* xh = c->x + h * c->N * c->d;
+        for (int j = 0; j < c->nq; j++) c->sse[h * c->nq + j] = 0.0;
+        const int64_t nblocks = c->axis == 3 ? c->N * (c->d / 32) : c->d * nb;
+        for (int64_t blk = 0; blk < nblocks; blk++) {
+            if (c->axis == 3) {
+                const int64_t r = blk / (c->d / 32), b = blk % (c->d / 32);
+                for (int i = 0; i < 32; i++) v[i] = bf16_bits_to_double(xh[r * c->d + b * 32 + i]);
+            } else {
+                const int64_t ch = blk / nb, b = blk % nb;
+                for (int i = 0; i < 32; i++) {
+                    const int64_t t = b * 32 + i;
+                    v[i] = t < c->N ? bf16_bits_to_double(xh[t * c->d + ch]) : 0.0;
+                }
+            }
+            for (int j = 0; j < c->nq; j++) {
+                uint8_t sc = quantize_block_qmax(v, 32, c->qs[j], cd);
+                double acc = 0.0;
+                for (int i = 0; i < 32; i++) {
+                    const double err = v[i] - mxref_decode(cd[i], sc);
+                    acc += err * err;
+                }
+                c->sse[h * c->nq + j] += acc;
+            }
+        }
+    }
+}
+
+int mxref_qmax_sse(const uint16_t* x, int64_t heads, int64_t N, int64_t d, int axis, const double* qs,
+                   int nq, double* sse, int nthreads) {
+    if (heads < 0 || N < 1 || d <= 0 || d % 32 != 0 || (axis != 2 && axis != 3) || nq < 1) return -1;
+    for (int j = 0; j < nq; j++)
+        if (!(qs[j] >= 4.0 && qs[j] <= 8.0)) return -1;
+    sse_ctx c = {x, N, d, axis, qs, nq, sse};
+    parallel_for(heads, nthreads, sse_range, &c);
     return 0;
 }
 

@@ -57,7 +57,7 @@ __global__ __launch_bounds__(256) void quantize_headdim_kernel(const uint4* __re
 
 // ---------------------------------------------------------------------------
 // Rotated head-dimension blocks (Q and K of the rotated mode): each row of 128
-// is multiplied by R_H = H/sqrt(128) (Sylvester Hadamard, Sec. 3.3, Algorithm
+// is multiplied by R_H = H/sqrt(128) (Sylvester Hadamard, Sec. 4.3, Algorithm
 // 2) before the block quantization above.  The product is the radix-2 fast
 // Walsh-Hadamard transform in fp32, stages h = 1, 2, 4, ..., 64, each mapping
 // (x[i], x[i+h]) (bit h of i clear) to (a + b, a - b), then one fp32 multiply

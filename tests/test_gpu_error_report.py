@@ -8,9 +8,9 @@ It checks the two claims the paper makes about these quantities:
 * PNQ's induced weights sum to one (Proposition 1);
 * direct placement loses mass on average (Sec. 3, "Normalization Mismatch in
   Online Softmax"), and UOS + PNQ brings the output's scale nearer to the
-  exact one than vanilla OCP does (the direction of the ablation, Sec. 5.3);
+  exact one than vanilla OCP does (the direction of the ablation, Sec. 5.4);
 * the Hadamard rotation of Q and K lowers the error where channels carry
-  outliers (its purpose in Sec. 3.3).
+  outliers (its purpose in Sec. 4.3).
 
 rel-L2 alone is dominated by the 4-bit quantization noise of V and P and does
 not separate the modes; the gain and the row sums do.

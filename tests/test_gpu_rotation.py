@@ -1,5 +1,5 @@
 """The rotated mode on the GPU (Q and K multiplied by R_H = H/sqrt(128)
-before MXFP4 quantization; Sec. 3.3, Algorithm 2).
+before MXFP4 quantization; Sec. 4.3, Algorithm 2).
 
 * Q/K codes and scales bit-exact against the oracle's fp32 fast Walsh-Hadamard
   transform + block quantizer: random rows over a wide range of magnitudes,

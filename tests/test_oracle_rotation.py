@@ -1,4 +1,4 @@
-"""Pins of the oracle's fixed Hadamard rotation R_H (Sec. 3.3, Algorithm 2:
+"""Pins of the oracle's fixed Hadamard rotation R_H (Sec. 4.3, Algorithm 2:
 Q^rot = Q R_H, K^rot = K R_H before quantization).
 
 * R_H = H / sqrt(128) with H the Sylvester Hadamard matrix: the image of every
