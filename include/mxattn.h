@@ -86,11 +86,14 @@ typedef enum {
     MXATTN_ERR_AXIS = 5,        /* block_axis is not 2 or 3                 */
     MXATTN_ERR_UNSUPPORTED = 6, /* d != 128                                 */
     MXATTN_ERR_OOM = 7,         /* workspace allocation failed              */
-    MXATTN_ERR_HIP = 8          /* a HIP call failed; see mxattn_last_error */
+    MXATTN_ERR_HIP = 8,         /* a HIP call failed; see mxattn_last_error */
+    MXATTN_ERR_BOUNDARY = 9     /* a scale boundary q outside [4, 8], or a
+                                   boundary count outside [1, 64]           */
 } mxattn_status;
 
 #define MXATTN_AXIS_TOKENS 2   /* blocks along N (V)      */
 #define MXATTN_AXIS_HEAD_DIM 3 /* blocks along d (Q and K) */
+#define MXATTN_MAX_BOUNDARIES 64 /* boundaries per mxattn_qmax_sse call */
 
 /* MXFP4-quantize a bf16 tensor x [B, H, N, d] (Algorithm 1 with the scale
  * rule of `mode`: OCP floor for MXATTN_OCP_VANILLA, UOS otherwise).  With
@@ -105,6 +108,38 @@ typedef enum {
  * Returns MXATTN_OK or an error status; nothing is launched on error. */
 int mxattn_quantize(const void* x, uint8_t* codes, uint8_t* scales, int block_axis, int mode,
                     int64_t B, int64_t H, int64_t N, int64_t d, void* stream);
+
+/* MXFP4-quantize with the ceil scale rule of a general boundary q: each
+ * block takes the smallest exponent e with M <= q 2^e (Eq. scale_definition,
+ * Eq. uos_mapping), clamped to [-127, 127].  q = 6 is TFS, q = 7 the OAS rule
+ * at 32-element blocks (App. "Relation to OAS and the OCP Endpoint
+ * Convention"), q = 7.25 UOS (identical to mxattn_quantize in a UOS mode) and
+ * q = 8 the ceil form of the OCP boundary (which differs from the floor rule
+ * of MXATTN_OCP_VANILLA only where M is a power of two).  Layouts, rounding
+ * and alignment as mxattn_quantize; no rotation.
+ *   qmax    the boundary q, 4 <= q <= 8 (MXATTN_ERR_BOUNDARY otherwise)
+ * Returns MXATTN_OK or an error status; nothing is launched on error. */
+int mxattn_quantize_qmax(const void* x, uint8_t* codes, uint8_t* scales, int block_axis, double qmax,
+                         int64_t B, int64_t H, int64_t N, int64_t d, void* stream);
+
+/* Per-(batch, head) sum of squared MXFP4 quantization errors
+ * sum_i (x_i - Q_q(x_i))^2 of x [B, H, N, d], blocked along block_axis, for
+ * each boundary qs[j] of the ceil rule above: the per-tensor MSE sweep of
+ * the paper's empirical check of the boundary (Sec. 5.5, Table
+ * cx_distribution, which sweeps q from 6.00 to 8.00 in steps of 0.05).
+ * Token blocks count their +0 padding, which adds no error.
+ *   x       device bf16 [B, H, N, d], 16-byte aligned, finite
+ *   qs      HOST array of nq boundaries, each 4 <= q <= 8, read before the
+ *           call returns; 1 <= nq <= MXATTN_MAX_BOUNDARIES
+ *   sse     device fp64 [B*H, nq], 8-byte aligned, written in full
+ * Sums are formed in fp64 (each element's squared error exactly); the order
+ * of additions within a workgroup is not fixed, so repeated calls may differ
+ * in the last bits.  Uses stream-ordered workspace (hipMallocAsync on
+ * `stream`): 2056 bytes per workgroup, about 2048 workgroups or one per
+ * (batch, head) if there are more, so about 2 KiB * max(B*H, 2048).
+ * Returns MXATTN_OK, MXATTN_ERR_OOM, or another error status. */
+int mxattn_qmax_sse(const void* x, int block_axis, const double* qs, int nq, double* sse, int64_t B,
+                    int64_t H, int64_t N, int64_t d, void* stream);
 
 /* MXFP4 attention forward O = softmax(Q K^T / sqrt(d)) V with MXFP4 Q, K, V
  * and MXFP4 P~ (Algorithm 2, with its Hadamard rotation in mode

@@ -78,6 +78,7 @@ const char* mxattn_status_string(int s) {
         case MXATTN_ERR_UNSUPPORTED: return "unsupported head dimension (d must be 128)";
         case MXATTN_ERR_OOM: return "workspace allocation failed";
         case MXATTN_ERR_HIP: return "HIP runtime error";
+        case MXATTN_ERR_BOUNDARY: return "invalid scale boundary (need 4 <= q <= 8 and 1 <= nq <= 64)";
         default: return "unknown status";
     }
 }
@@ -118,6 +119,55 @@ int mxattn_quantize(const void* x, uint8_t* codes, uint8_t* scales, int block_ax
         return MXATTN_ERR_HIP;
     }
     return MXATTN_OK;
+}
+
+int mxattn_quantize_qmax(const void* x, uint8_t* codes, uint8_t* scales, int block_axis, double qmax,
+                         int64_t B, int64_t H, int64_t N, int64_t d, void* stream) {
+    if (!x || !codes || !scales) return MXATTN_ERR_NULL;
+    if (block_axis != MXATTN_AXIS_HEAD_DIM && block_axis != MXATTN_AXIS_TOKENS) return MXATTN_ERR_AXIS;
+    if (!(qmax >= 4.0 && qmax <= 8.0)) return MXATTN_ERR_BOUNDARY;
+    if (int st = check_shape(B, H, N, d)) return st;
+    if (!aligned(x, 16) || !aligned(codes, 16)) return MXATTN_ERR_ALIGN;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    hipError_t e = block_axis == MXATTN_AXIS_HEAD_DIM
+                       ? mxattn::launch_quantize_headdim(x, codes, scales, B * H * N, mxattn::kRuleQmax, s, qmax)
+                       : mxattn::launch_quantize_tokens(x, codes, scales, B * H, N, mxattn::kRuleQmax, s, qmax);
+    if (e != hipSuccess) {
+        set_error("quantize launch", e);
+        return MXATTN_ERR_HIP;
+    }
+    return MXATTN_OK;
+}
+
+int mxattn_qmax_sse(const void* x, int block_axis, const double* qs, int nq, double* sse, int64_t B,
+                    int64_t H, int64_t N, int64_t d, void* stream) {
+    if (!x || !qs || !sse) return MXATTN_ERR_NULL;
+    if (block_axis != MXATTN_AXIS_HEAD_DIM && block_axis != MXATTN_AXIS_TOKENS) return MXATTN_ERR_AXIS;
+    if (nq < 1 || nq > MXATTN_MAX_BOUNDARIES) return MXATTN_ERR_BOUNDARY;
+    for (int j = 0; j < nq; j++)
+        if (!(qs[j] >= 4.0 && qs[j] <= 8.0)) return MXATTN_ERR_BOUNDARY;
+    if (int st = check_shape(B, H, N, d)) return st;
+    if (!aligned(x, 16) || !aligned(sse, 8)) return MXATTN_ERR_ALIGN;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    keep_pool_memory();
+    void* ws = nullptr;
+    hipError_t e = hipMallocAsync(&ws, (size_t)mxattn::qmax_sse_workspace_bytes(block_axis, B * H, N), s);
+    if (e != hipSuccess || !ws) {
+        set_error("hipMallocAsync", e);
+        return MXATTN_ERR_OOM;
+    }
+    int st = MXATTN_OK;
+    e = mxattn::launch_qmax_sse(x, block_axis, qs, nq, sse, ws, B * H, N, s);
+    if (e != hipSuccess) {
+        set_error("sse sweep launch", e);
+        st = MXATTN_ERR_HIP;
+    }
+    e = hipFreeAsync(ws, s);
+    if (st == MXATTN_OK && e != hipSuccess) {
+        set_error("hipFreeAsync", e);
+        st = MXATTN_ERR_HIP;
+    }
+    return st;
 }
 
 // Rearranges the K^/V^ scales into sc (mxattn::tile_scales_bytes(B*H, Nkv)
@@ -238,8 +288,10 @@ int mxattn_cross_forward(const void* q, const void* k, const void* v, void* out,
 
     const int rule = rule_of(mode);
     int st = MXATTN_OK;
-    auto qk = mode == MXATTN_UOS_PNQ_ROT ? mxattn::launch_quantize_headdim_rotated
-                                         : mxattn::launch_quantize_headdim;
+    auto qk = [mode](const void* x, uint8_t* c, uint8_t* sc, int64_t rows, int rule, hipStream_t st) {
+        return mode == MXATTN_UOS_PNQ_ROT ? mxattn::launch_quantize_headdim_rotated(x, c, sc, rows, rule, st)
+                                          : mxattn::launch_quantize_headdim(x, c, sc, rows, rule, st);
+    };
     if ((e = qk(q, qc, qs, B * H * Nq, rule, s)) != hipSuccess ||
         (e = qk(k, kc, ks, B * H * Nkv, rule, s)) != hipSuccess ||
         (e = mxattn::launch_quantize_tokens(v, vc, vs, B * H, Nkv, rule, s)) != hipSuccess) {

@@ -43,6 +43,37 @@ __device__ __forceinline__ int scale_exponent_bf16(uint32_t mbits) {
     return e < -127 ? -127 : e;
 }
 
+// Ceil rule with a general boundary 4 <= q <= 8 (Eq. scale_definition): the
+// smallest e with M <= q 2^e, clamped to [-127, 127].  With the bf16 maximum
+// M = (1 + F/128) 2^(E-127), e = E - 129 exactly when 1 + F/128 <= q/4, i.e.
+// F <= 32 (q - 4); otherwise E - 128 (1 + F/128 < 2 <= q/2).  A power of two
+// (F = 0) also satisfies 1 <= q/8 when q = 8 and takes E - 130.  The host
+// passes thr = floor(32 (q - 4)) (exact for a binary64 q in [4, 8]) and
+// pow2_down = (q == 8).  bf16 maxima below 2^-126 clamp to -127 as above.
+struct Boundary {
+    int thr;
+    int pow2_down;
+};
+
+// Host side: the Boundary of q (defined in quantize.hip).
+Boundary boundary_of(double q);
+
+__device__ __forceinline__ int scale_exponent_bf16_q(uint32_t mbits, Boundary b) {
+    const int E = (int)(mbits >> 7);
+    if (E == 0) return -127;
+    const int F = (int)(mbits & 0x7Fu);
+    int e = E - 129 + (F > b.thr ? 1 : 0) - ((F == 0 && b.pow2_down) ? 1 : 0);
+    return e < -127 ? -127 : (e > 127 ? 127 : e);
+}
+
+template <int kRule>
+__device__ __forceinline__ int block_exponent_bf16(uint32_t mbits, Boundary b) {
+    if constexpr (kRule == kRuleQmax)
+        return scale_exponent_bf16_q(mbits, b);
+    else
+        return scale_exponent_bf16<kRule>(mbits);
+}
+
 // The fp32 whose exponent field is the E8M0 byte: the scale operand of the
 // gfx950 FP4 conversions, which divide by 2^(exponent field - 127).
 __device__ __forceinline__ float e8m0_as_f32(uint32_t byte) {

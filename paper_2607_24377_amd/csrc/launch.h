@@ -7,7 +7,9 @@
 namespace mxattn {
 
 // Shared-scale rule of the MXFP4 quantizer.
-enum Rule { kRuleOcp = 0, kRuleUos = 1 };
+// kRuleQmax is the ceil rule of a general boundary q (Boundary in
+// device_common.h), a run-time argument of the quantizers.
+enum Rule { kRuleOcp = 0, kRuleUos = 1, kRuleQmax = 2 };
 
 // Query rows per workgroup of the fused attention kernel, and its KV tile
 // B_c: the running maximum is updated once per kKvTile keys.
@@ -15,14 +17,22 @@ constexpr int kQueryTile = 128;
 constexpr int kKvTile = 128;
 
 hipError_t launch_quantize_headdim(const void* x, uint8_t* codes, uint8_t* scales, int64_t rows,
-                                   int rule, hipStream_t stream);
+                                   int rule, hipStream_t stream, double qmax = 0.0);
 
 // Q/K of the rotated mode: rows multiplied by R_H = H/sqrt(128) first.
 hipError_t launch_quantize_headdim_rotated(const void* x, uint8_t* codes, uint8_t* scales, int64_t rows,
                                            int rule, hipStream_t stream);
 
 hipError_t launch_quantize_tokens(const void* x, uint8_t* codes, uint8_t* scales, int64_t BH,
-                                  int64_t N, int rule, hipStream_t stream);
+                                  int64_t N, int rule, hipStream_t stream, double qmax = 0.0);
+
+// Per-head squared-error sweep over boundaries (qmax.hip).  The histogram
+// pass writes partial sums to a workspace of qmax_sse_workspace_bytes(...)
+// bytes; the reduction turns them into sse[BH, nq] (fp64).
+constexpr int kMaxBoundaries = 64;
+int64_t qmax_sse_workspace_bytes(int axis, int64_t BH, int64_t N);
+hipError_t launch_qmax_sse(const void* x, int axis, const double* qs, int nq, double* sse,
+                           void* workspace, int64_t BH, int64_t N, hipStream_t stream);
 
 struct AttnArgs {
     const uint8_t* qc;  // [BH, Nq, 64]

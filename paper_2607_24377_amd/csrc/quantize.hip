@@ -1,11 +1,13 @@
 // quantize.hip -- MXFP4 block quantizers for gfx950 (Algorithm 1 with the UOS
-// or the OCP floor scale rule).
+// rule, the OCP floor scale rule, or the ceil rule of a general boundary q).
 //
 // Both kernels stream bf16 from HBM once and write 4-bit codes plus one E8M0
 // byte per 32 elements (2.53125 bytes of traffic per element).  The E2M1
 // rounding itself is done by the gfx950 scaled FP4 conversion, which rounds to
 // nearest with ties to the even code, saturates at +-6 and keeps the sign bit
 // (the same readings the library documents for the quantizer).
+#include <cmath>
+
 #include "device_common.h"
 #include "launch.h"
 
@@ -20,7 +22,7 @@ template <int kRule>
 __global__ __launch_bounds__(256) void quantize_headdim_kernel(const uint4* __restrict__ x,
                                                                uint32_t* __restrict__ codes,
                                                                uint8_t* __restrict__ scales,
-                                                               int64_t n_chunks) {
+                                                               int64_t n_chunks, Boundary bq) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     const bool valid = i < n_chunks;
     uint4 v = make_uint4(0, 0, 0, 0);
@@ -41,7 +43,7 @@ __global__ __launch_bounds__(256) void quantize_headdim_kernel(const uint4* __re
     m = max(m, (uint32_t)__shfl_xor((int)m, 2));
 
     // all-zero block: sigma = 1 (Algorithm 1); codes come out as signed zeros
-    const uint32_t sbyte = (m == 0) ? 127u : (uint32_t)(scale_exponent_bf16<kRule>(m) + 127);
+    const uint32_t sbyte = (m == 0) ? 127u : (uint32_t)(block_exponent_bf16<kRule>(m, bq) + 127);
     const float sf = e8m0_as_f32(sbyte);
 
     uint32_t c = 0;
@@ -142,7 +144,7 @@ template <int kRule>
 __global__ __launch_bounds__(256) void quantize_tokens_kernel(const uint4* __restrict__ x,
                                                               uint8_t* __restrict__ codes,
                                                               uint8_t* __restrict__ scales, int N,
-                                                              int nb, int groups) {
+                                                              int nb, int groups, Boundary bq) {
     __shared__ uint32_t tile[kVqTokens * 64];  // [token][64 dwords = 128 bf16]
     const int tid = threadIdx.x;
     const int bh = blockIdx.x / groups;
@@ -174,8 +176,8 @@ __global__ __launch_bounds__(256) void quantize_tokens_kernel(const uint4* __res
         m0 = max(m0, d & 0x7FFFu);
         m1 = max(m1, (d >> 16) & 0x7FFFu);
     }
-    const uint32_t s0 = (m0 == 0) ? 127u : (uint32_t)(scale_exponent_bf16<kRule>(m0) + 127);
-    const uint32_t s1 = (m1 == 0) ? 127u : (uint32_t)(scale_exponent_bf16<kRule>(m1) + 127);
+    const uint32_t s0 = (m0 == 0) ? 127u : (uint32_t)(block_exponent_bf16<kRule>(m0, bq) + 127);
+    const uint32_t s1 = (m1 == 0) ? 127u : (uint32_t)(block_exponent_bf16<kRule>(m1, bq) + 127);
     const float f0 = e8m0_as_f32(s0), f1 = e8m0_as_f32(s1);
 
     uint32_t c0[4] = {0, 0, 0, 0}, c1[4] = {0, 0, 0, 0};
@@ -211,17 +213,29 @@ __global__ __launch_bounds__(256) void quantize_tokens_kernel(const uint4* __res
     scales[(row0 + 1) * nb + blk] = (uint8_t)s1;
 }
 
+// Kernel argument of the kRuleQmax rule for boundary q (4 <= q <= 8).
+Boundary boundary_of(double q) {
+    Boundary b;
+    b.thr = (int)std::floor(32.0 * (q - 4.0));
+    b.pow2_down = q == 8.0 ? 1 : 0;
+    return b;
+}
+
 hipError_t launch_quantize_headdim(const void* x, uint8_t* codes, uint8_t* scales, int64_t rows,
-                                   int rule, hipStream_t stream) {
+                                   int rule, hipStream_t stream, double qmax) {
     const int64_t n_chunks = rows * 16;  // d = 128: 16 chunks of 8 elements per row
     if (n_chunks == 0) return hipSuccess;
     const dim3 grid((unsigned)((n_chunks + 255) / 256));
+    const Boundary bq = boundary_of(rule == kRuleQmax ? qmax : 7.25);
     if (rule == kRuleUos)
         quantize_headdim_kernel<kRuleUos><<<grid, 256, 0, stream>>>(
-            (const uint4*)x, (uint32_t*)codes, scales, n_chunks);
+            (const uint4*)x, (uint32_t*)codes, scales, n_chunks, bq);
+    else if (rule == kRuleQmax)
+        quantize_headdim_kernel<kRuleQmax><<<grid, 256, 0, stream>>>(
+            (const uint4*)x, (uint32_t*)codes, scales, n_chunks, bq);
     else
         quantize_headdim_kernel<kRuleOcp><<<grid, 256, 0, stream>>>(
-            (const uint4*)x, (uint32_t*)codes, scales, n_chunks);
+            (const uint4*)x, (uint32_t*)codes, scales, n_chunks, bq);
     return hipGetLastError();
 }
 
@@ -240,16 +254,20 @@ hipError_t launch_quantize_headdim_rotated(const void* x, uint8_t* codes, uint8_
 }
 
 hipError_t launch_quantize_tokens(const void* x, uint8_t* codes, uint8_t* scales, int64_t BH,
-                                  int64_t N, int rule, hipStream_t stream) {
+                                  int64_t N, int rule, hipStream_t stream, double qmax) {
     const int nb = (int)((N + 31) / 32);
     const int groups = (int)((N + kVqTokens - 1) / kVqTokens);
     const dim3 grid((unsigned)(BH * groups));
+    const Boundary bq = boundary_of(rule == kRuleQmax ? qmax : 7.25);
     if (rule == kRuleUos)
         quantize_tokens_kernel<kRuleUos><<<grid, 256, 0, stream>>>((const uint4*)x, codes, scales,
-                                                                    (int)N, nb, groups);
+                                                                    (int)N, nb, groups, bq);
+    else if (rule == kRuleQmax)
+        quantize_tokens_kernel<kRuleQmax><<<grid, 256, 0, stream>>>((const uint4*)x, codes, scales,
+                                                                     (int)N, nb, groups, bq);
     else
         quantize_tokens_kernel<kRuleOcp><<<grid, 256, 0, stream>>>((const uint4*)x, codes, scales,
-                                                                    (int)N, nb, groups);
+                                                                    (int)N, nb, groups, bq);
     return hipGetLastError();
 }
 

@@ -45,6 +45,11 @@ def lib() -> ctypes.CDLL:
             P, I, I64, SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t
             L.mxattn_quantize.argtypes = [P, P, P, I, I, I64, I64, I64, I64, P]
             L.mxattn_quantize.restype = I
+            D = ctypes.c_double
+            L.mxattn_quantize_qmax.argtypes = [P, P, P, I, D, I64, I64, I64, I64, P]
+            L.mxattn_quantize_qmax.restype = I
+            L.mxattn_qmax_sse.argtypes = [P, I, P, I, P, I64, I64, I64, I64, P]
+            L.mxattn_qmax_sse.restype = I
             L.mxattn_forward.argtypes = [P, P, P, P, I64, I64, I64, I64, I, P]
             L.mxattn_forward.restype = I
             L.mxattn_attend.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I, P]
@@ -122,6 +127,33 @@ def quantize(x: torch.Tensor, block_axis: int, mode, stream=None, codes=None, sc
                                _mode(mode), B, H, N, d, _stream(stream))
     _check(st, "mxattn_quantize")
     return codes, scales
+
+
+def quantize_qmax(x: torch.Tensor, block_axis: int, qmax: float, stream=None, codes=None, scales=None):
+    """MXFP4-quantize bf16 x [B, H, N, d] with the ceil rule of boundary qmax."""
+    B, H, N, d = _bhnd(x)
+    cs, ss = code_shapes(block_axis, B, H, N, d)
+    if codes is None:
+        codes = torch.empty(cs, dtype=torch.uint8, device=x.device)
+    if scales is None:
+        scales = torch.empty(ss, dtype=torch.uint8, device=x.device)
+    st = lib().mxattn_quantize_qmax(x.data_ptr(), codes.data_ptr(), scales.data_ptr(), block_axis,
+                                    float(qmax), B, H, N, d, _stream(stream))
+    _check(st, "mxattn_quantize_qmax")
+    return codes, scales
+
+
+def qmax_sse(x: torch.Tensor, block_axis: int, qs, stream=None, out=None):
+    """Per-(batch, head) sum of squared MXFP4 errors of bf16 x [B, H, N, d] for
+    each boundary in qs; returns a float64 device tensor [B*H, len(qs)]."""
+    B, H, N, d = _bhnd(x)
+    q = (ctypes.c_double * len(qs))(*[float(v) for v in qs])
+    if out is None:
+        out = torch.empty((B * H, len(qs)), dtype=torch.float64, device=x.device)
+    st = lib().mxattn_qmax_sse(x.data_ptr(), block_axis, ctypes.cast(q, ctypes.c_void_p), len(qs),
+                               out.data_ptr(), B, H, N, d, _stream(stream))
+    _check(st, "mxattn_qmax_sse")
+    return out
 
 
 def forward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, mode, out=None, stream=None):

@@ -31,6 +31,7 @@ def L():
 def test_header_declares_the_entry_points():
     names = _declared_functions()
     for n in ["mxattn_quantize", "mxattn_forward", "mxattn_attend", "mxattn_codes_bytes",
+              "mxattn_quantize_qmax", "mxattn_qmax_sse",
               "mxattn_scales_bytes", "mxattn_kv_tile", "mxattn_status_string",
               "mxattn_last_error"]:
         assert n in names
@@ -108,3 +109,26 @@ def test_forward_and_attend_reject_bad_arguments(L):
     bad = list(args)
     bad[1] = FAKE + 1  # q_scales may have any alignment: only the shape error fires
     assert a(*bad, 1, 1, 0, 128, 0, None) == 2
+
+
+def test_boundary_entry_points_reject_bad_arguments(L):
+    q = L.mxattn_quantize_qmax
+    assert q(FAKE, FAKE, FAKE, 3, 7.25, 1, 1, 0, 128, None) == 2       # shape: valid q
+    assert q(None, FAKE, FAKE, 3, 7.25, 1, 1, 8, 128, None) == 1
+    assert q(FAKE, FAKE, FAKE, 1, 7.25, 1, 1, 8, 128, None) == 5
+    for bad in (3.999, 8.001, float("nan"), float("inf"), -7.25):
+        assert q(FAKE, FAKE, FAKE, 3, bad, 1, 1, 8, 128, None) == 9    # BOUNDARY
+    assert q(FAKE, FAKE, FAKE, 2, 4.0, 1, 1, 8, 64, None) == 6         # q = 4 and 8 are valid
+    assert q(FAKE, FAKE + 4, FAKE, 3, 8.0, 1, 1, 8, 128, None) == 3
+    s = L.mxattn_qmax_sse
+    qs = (ctypes.c_double * 65)(*([7.0] * 65))
+    assert s(FAKE, 3, qs, 41, FAKE, 1, 1, 0, 128, None) == 2
+    assert s(FAKE, 3, None, 1, FAKE, 1, 1, 8, 128, None) == 1
+    assert s(FAKE, 3, qs, 1, None, 1, 1, 8, 128, None) == 1
+    assert s(FAKE, 4, qs, 1, FAKE, 1, 1, 8, 128, None) == 5
+    assert s(FAKE, 3, qs, 0, FAKE, 1, 1, 8, 128, None) == 9
+    assert s(FAKE, 3, qs, 65, FAKE, 1, 1, 8, 128, None) == 9
+    bad = (ctypes.c_double * 3)(6.0, 8.5, 7.0)
+    assert s(FAKE, 2, bad, 3, FAKE, 1, 1, 8, 128, None) == 9
+    assert s(FAKE, 3, qs, 64, FAKE + 4, 1, 1, 8, 128, None) == 3       # sse needs 8 bytes
+    assert s(FAKE, 3, qs, 64, FAKE, 1, 1, 8, 96, None) == 6
