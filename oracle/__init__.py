@@ -83,6 +83,10 @@ def lib() -> ctypes.CDLL:
             L.mxref_quantize_rows_qmax.restype = I
             L.mxref_qmax_sse.argtypes = [P, I64, I64, I64, I, P, I, P, I]
             L.mxref_qmax_sse.restype = I
+            L.mxref_softmax_rows.argtypes = [P, P, I64, I64, I64, P, I]
+            L.mxref_softmax_rows.restype = I
+            L.mxref_rowsum_diag.argtypes = [P, I64, I64, I64, I, ctypes.c_float, P, I]
+            L.mxref_rowsum_diag.restype = I
             L.mxref_hadamard_f32.argtypes = [P, I64]
             L.mxref_hadamard_f32.restype = None
             L.mxref_quantize_keys.argtypes = [P, I64, I64, I64, I, P, P, I]
@@ -197,6 +201,31 @@ def qmax_sse(x_bits: np.ndarray, axis: int, qs, nthreads: int = 0) -> np.ndarray
     q = np.ascontiguousarray(np.asarray(qs, dtype=np.float64))
     out = np.empty((heads, q.size), dtype=np.float64)
     if lib().mxref_qmax_sse(_ptr(x), heads, N, d, axis, _ptr(q), q.size, _ptr(out), nthreads) != 0:
+        raise ValueError("bad arguments")
+    return out
+
+
+DIAG_FIELDS = ("rowsum", "mass", "zeroing", "saturation", "down", "up", "exact", "entropy")
+
+
+def softmax_rows(q: np.ndarray, k: np.ndarray, nthreads: int = 0) -> np.ndarray:
+    """Exact fp64 softmax(q k^T / sqrt(d)) rows; q [rows, d], k [N, d] (float)."""
+    qd = np.ascontiguousarray(q, dtype=np.float64)
+    kd = np.ascontiguousarray(k, dtype=np.float64)
+    out = np.empty((qd.shape[0], kd.shape[0]), dtype=np.float64)
+    if lib().mxref_softmax_rows(_ptr(qd), _ptr(kd), kd.shape[0], kd.shape[1], qd.shape[0], _ptr(out),
+                                nthreads) != 0:
+        raise ValueError("bad arguments")
+    return out
+
+
+def rowsum_diag(P: np.ndarray, N: int, rule: int, gamma: float = 1.0, nthreads: int = 0) -> np.ndarray:
+    """Per-row diagnostics of MXFP4-quantizing fp32 probability rows P [rows, ld]
+    (first N entries valid); returns [rows, 8] fp64 in DIAG_FIELDS order."""
+    p = np.ascontiguousarray(P, dtype=np.float32)
+    rows, ld = p.shape
+    out = np.empty((rows, 8), dtype=np.float64)
+    if lib().mxref_rowsum_diag(_ptr(p), rows, N, ld, rule, float(gamma), _ptr(out), nthreads) != 0:
         raise ValueError("bad arguments")
     return out
 

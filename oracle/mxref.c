@@ -27,6 +27,10 @@
  *     App. "Relation to OAS and the OCP Endpoint Convention"), UOS (7.25) and
  *     the ceil form of OCP (8); the per-head squared-error sweep over q of
  *     the empirical check in Sec. 5.5 (Table cx_distribution).
+ *   - Row-sum diagnostics of block-quantized materialized probabilities:
+ *     Sec. 5.5 ("Validation of Pre-Normalization Quantization", Fig.
+ *     pnq_rowsum): per-row quantized mass, its split into zeroing,
+ *     saturation, downward and upward rounding, and the row entropy.
  *   - Online softmax recurrence: Sec. 2 Eqs. online_attention /
  *     online_attention_output; direct placement: Eq. direct_mxfp4_tile;
  *     PNQ: Eqs. pnq_tile_contribution / pnq_online_update; Algorithm 2
@@ -728,6 +732,122 @@ int mxref_attention_exact_rows(const double* qrows, const double* keys, const do
     if (N <= 0 || d <= 0 || n_rows < 0) return -1;
     exact_ctx E = {qrows, keys, vals, N, d, out};
     parallel_for(n_rows, nthreads, exact_range, &E);
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* Row-sum diagnostics on materialized probabilities (Sec. 5.5,         */
+/* "Validation of Pre-Normalization Quantization", Fig. pnq_rowsum)     */
+/* ------------------------------------------------------------------ */
+
+/* Exact softmax rows P[r, n] = softmax_n(q_r . k_n / sqrt(d)) in fp64 (Eq.
+ * standard_attention without the product with V). */
+typedef struct {
+    const double* q;
+    const double* k;
+    int64_t N, d;
+    double* P;
+} softmax_ctx;
+
+static void softmax_range(void* p, int64_t r0, int64_t r1) {
+    softmax_ctx* C = (softmax_ctx*)p;
+    const int64_t N = C->N, d = C->d;
+    const double scale = 1.0 / sqrt((double)d);
+    for (int64_t r = r0; r < r1; r++) {
+        const double* qr = C->q + r * d;
+        double* prow = C->P + r * N;
+        double mx = -INFINITY;
+        for (int64_t n = 0; n < N; n++) {
+            double acc = 0.0;
+            for (int64_t c = 0; c < d; c++) acc += qr[c] * C->k[n * d + c];
+            prow[n] = acc * scale;
+            if (prow[n] > mx) mx = prow[n];
+        }
+        double sum = 0.0;
+        for (int64_t n = 0; n < N; n++) {
+            prow[n] = exp(prow[n] - mx);
+            sum += prow[n];
+        }
+        for (int64_t n = 0; n < N; n++) prow[n] /= sum;
+    }
+}
+
+int mxref_softmax_rows(const double* qrows, const double* keys, int64_t N, int64_t d, int64_t n_rows,
+                       double* P, int nthreads) {
+    if (N <= 0 || d <= 0 || n_rows < 0) return -1;
+    softmax_ctx C = {qrows, keys, N, d, P};
+    parallel_for(n_rows, nthreads, softmax_range, &C);
+    return 0;
+}
+
+/* What block-wise MXFP4 quantization does to the mass of each row of a
+ * materialized probability matrix (the diagnostic of Fig. pnq_rowsum).
+ * P is fp32 [rows, ld], N valid entries per row (p >= 0), blocks of 32
+ * consecutive entries from the row start, the last one padded with +0.
+ * Each entry is pre-scaled x = fl32(gamma * p) (the "pre-quant global
+ * scaling" baseline of Fig. pnq_rowsum (C); gamma = 1 is plain
+ * quantization), quantized with the block's scale rule to Q(x), and
+ * contributes Q(x) * g - p with g = fl64(1 / gamma).  Entries fall in one of
+ *   zeroing     p > 0 and Q(x) = 0
+ *   saturation  x / sigma > 6 (above the largest E2M1 magnitude)
+ *   down        0 < Q(x) < x otherwise
+ *   up          Q(x) > x
+ *   exact       Q(x) = x
+ * stats[r] = {sum_j Q(x_j) g, sum_j p_j, zeroing, saturation, down, up,
+ * exact, -sum_{p_j > 0} p_j ln p_j}; the row sum minus the mass equals the
+ * sum of the five contributions. */
+typedef struct {
+    const float* P;
+    int64_t N, ld;
+    int rule;
+    float gamma;
+    double* stats;
+} diag_ctx;
+
+static void diag_range(void* p, int64_t r0, int64_t r1) {
+    diag_ctx* C = (diag_ctx*)p;
+    const double g = 1.0 / (double)C->gamma;
+    double x[32];
+    uint8_t cd[32];
+    for (int64_t r = r0; r < r1; r++) {
+        const float* prow = C->P + r * C->ld;
+        double st[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        for (int64_t b = 0; b < C->N; b += 32) {
+            const int n = (int)((C->N - b) < 32 ? (C->N - b) : 32);
+            for (int i = 0; i < n; i++) x[i] = (double)(float)(C->gamma * prow[b + i]);
+            const uint8_t sc = quantize_block(x, n, C->rule, cd);
+            const double sigma = ldexp(1.0, (int)sc - 127);
+            for (int i = 0; i < n; i++) {
+                const double pj = (double)prow[b + i];
+                const double qx = mxref_decode(cd[i], sc);
+                const double c = qx * g - pj;
+                int cls;
+                if (pj > 0.0 && (cd[i] & 7) == 0)
+                    cls = 2;
+                else if (x[i] > 6.0 * sigma)
+                    cls = 3;
+                else if (qx < x[i])
+                    cls = 4;
+                else if (qx > x[i])
+                    cls = 5;
+                else
+                    cls = 6;
+                st[0] += qx * g;
+                st[1] += pj;
+                st[cls] += c;
+                if (pj > 0.0) st[7] -= pj * log(pj);
+            }
+        }
+        memcpy(C->stats + r * 8, st, sizeof st);
+    }
+}
+
+int mxref_rowsum_diag(const float* P, int64_t rows, int64_t N, int64_t ld, int rule, float gamma,
+                      double* stats, int nthreads) {
+    if (rows < 0 || N < 1 || ld < N || (rule != RULE_OCP && rule != RULE_UOS) || !(gamma > 0.0f))
+        return -1;
+    diag_ctx C = {P, N, ld, rule, gamma, stats};
+    parallel_for(rows, nthreads, diag_range, &C);
     return 0;
 }
 
