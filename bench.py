@@ -115,6 +115,8 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=0, help="oracle sample rows (0: ~15 s)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-overhead", action="store_true")
+    ap.add_argument("--no-next", action="store_true",
+                    help="skip the boundary-sweep timings (the scope table's next rows)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -173,6 +175,24 @@ def main():
         "quantize_headdim_GBps": elems * 2.53125 / (quant_q_ms * 1e-3) / 1e9,
         "quantize_tokens_GBps": w.B * w.H * w.n_kv * w.d * 2.53125 / (quant_ms * 1e-3) / 1e9,
     }
+    if not args.no_next:
+        # the boundary family and the 41-point MSE sweep of Table cx_distribution
+        sweep = [round(6.0 + 0.05 * i, 2) for i in range(41)]
+        sse = torch.empty((w.B * w.H, len(sweep)), dtype=torch.float64, device=dev)
+        log("[bench] timing the boundary quantizer and the MSE sweep")
+        qq_ms = time_ms(lambda: mxattn.quantize_qmax(q, mxattn.AXIS_HEAD_DIM, 7.0, codes=qc, scales=qs),
+                        args.steps, 1, torch)
+        sq_ms = time_ms(lambda: mxattn.qmax_sse(q, mxattn.AXIS_HEAD_DIM, sweep, out=sse), args.steps, 1, torch)
+        sv_ms = time_ms(lambda: mxattn.qmax_sse(v, mxattn.AXIS_TOKENS, sweep, out=sse), args.steps, 1, torch)
+        extra["boundary_sweep"] = {
+            "boundaries": len(sweep),
+            "quantize_qmax_headdim_ms": qq_ms,
+            "sse_headdim_ms": sq_ms,
+            "sse_tokens_ms": sv_ms,
+            "sse_headdim_GBps": elems * 2.0 / (sq_ms * 1e-3) / 1e9,
+            "sse_tokens_GBps": w.B * w.H * w.n_kv * w.d * 2.0 / (sv_ms * 1e-3) / 1e9,
+        }
+        del sse
     if not args.no_overhead:
         other = "ocp_vanilla" if args.mode != "ocp_vanilla" else "uos_pnq"
         log(f"[bench] timing forward {other} for the overhead comparison")
