@@ -25,6 +25,7 @@ if ROOT not in sys.path:
 
 METRIC = "MXFP4 attn fwd TFLOPS (4·B·H·N²·d/t) & % of MXFP4 MFMA peak, N=75600"
 PEAK_FP4_TFLOPS = 10100.0  # MI355X dense MXFP4 matrix-core peak, 10.1 PFLOP/s
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 matrix-core peak, 2.5 PFLOP/s
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attention_video720p_hbm_traffic.json")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_24377_amd", "csrc", "attention.hip")
 
@@ -193,6 +194,28 @@ def main():
             "sse_tokens_GBps": w.B * w.H * w.n_kv * w.d * 2.0 / (sv_ms * 1e-3) / 1e9,
         }
         del sse
+        # row-sum diagnostics (Fig. pnq_rowsum): the fused whole-tensor pass
+        # and, on a materialized 128-row tile of P, the standalone quantizer
+        log("[bench] timing the row-sum diagnostics")
+        stats = torch.empty((w.B, w.H, w.N, 8), dtype=torch.float64, device=dev)
+        fused_ms = time_ms(lambda: mxattn.attention_rowsum_diag(q, k, args.mode, out=stats),
+                           max(1, args.steps // 5), 1, torch)
+        rows = min(128, w.N)
+        P = mxattn.softmax_rows(q, k, 0, rows)
+        tile_stats = torch.empty((w.B * w.H * rows, 8), dtype=torch.float64, device=dev)
+        soft_ms = time_ms(lambda: mxattn.softmax_rows(q, k, 0, rows, out=P), args.steps, 1, torch)
+        diag_ms = time_ms(lambda: mxattn.rowsum_diag(P, w.n_kv, args.mode, out=tile_stats), args.steps, 1, torch)
+        score_flops = 2 * 2.0 * w.B * w.H * w.N * w.n_kv * w.d  # two passes of Q K^T
+        extra["rowsum_diag"] = {
+            "fused_ms": fused_ms,
+            "fused_score_TFLOPs": score_flops / (fused_ms * 1e-3) / 1e12,
+            "fused_frac_of_bf16_peak": score_flops / (fused_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+            "tile_rows": rows,
+            "softmax_rows_tile_ms": soft_ms,
+            "diag_tile_ms": diag_ms,
+            "diag_tile_GBps": P.numel() * 4 / (diag_ms * 1e-3) / 1e9,
+        }
+        del stats, P, tile_stats
     if not args.no_overhead:
         other = "ocp_vanilla" if args.mode != "ocp_vanilla" else "uos_pnq"
         log(f"[bench] timing forward {other} for the overhead comparison")

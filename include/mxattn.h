@@ -87,8 +87,9 @@ typedef enum {
     MXATTN_ERR_UNSUPPORTED = 6, /* d != 128                                 */
     MXATTN_ERR_OOM = 7,         /* workspace allocation failed              */
     MXATTN_ERR_HIP = 8,         /* a HIP call failed; see mxattn_last_error */
-    MXATTN_ERR_BOUNDARY = 9     /* a scale boundary q outside [4, 8], or a
-                                   boundary count outside [1, 64]           */
+    MXATTN_ERR_BOUNDARY = 9     /* a scale boundary q outside [4, 8], a
+                                   boundary count outside [1, 64], or a
+                                   pre-scale gamma not in (0, 3e38)         */
 } mxattn_status;
 
 #define MXATTN_AXIS_TOKENS 2   /* blocks along N (V)      */
@@ -140,6 +141,55 @@ int mxattn_quantize_qmax(const void* x, uint8_t* codes, uint8_t* scales, int blo
  * Returns MXATTN_OK, MXATTN_ERR_OOM, or another error status. */
 int mxattn_qmax_sse(const void* x, int block_axis, const double* qs, int nq, double* sse, int64_t B,
                     int64_t H, int64_t N, int64_t d, void* stream);
+
+/* Row-sum diagnostics of MXFP4-quantized attention probabilities (Sec. 5.5,
+ * "Validation of Pre-Normalization Quantization", Fig. pnq_rowsum): what
+ * direct block quantization of a materialized, normalized P does to the mass
+ * of each row, which PNQ avoids.  Per row, stats holds 8 fp64 values
+ *   [0] sum_j Q(x_j) / gamma        the row sum after quantization
+ *   [1] sum_j p_j                    the row sum before
+ *   [2] zeroing     sum of Q(x_j)/gamma - p_j over p_j > 0 with Q(x_j) = 0
+ *   [3] saturation  ... over x_j / sigma > 6 (above the largest E2M1 value)
+ *   [4] down        ... over the other entries with Q(x_j) < x_j
+ *   [5] up          ... over Q(x_j) > x_j
+ *   [6] exact       ... over Q(x_j) = x_j
+ *   [7] entropy     -sum_{p_j > 0} p_j ln p_j (nats)
+ * with x_j = fp32(gamma * p_j) quantized in blocks of 32 consecutive entries
+ * of the row (the last block padded with +0) by the scale rule of `mode`
+ * (OCP floor for MXATTN_OCP_VANILLA, UOS otherwise), and 1/gamma rounded to
+ * fp64.  gamma is the single "pre-quant global scaling" factor of
+ * Fig. pnq_rowsum (C); gamma = 1 quantizes P as it is.  [0] - [1] equals
+ * [2] + ... + [6] up to rounding.  Sums are fp64 (each term exact but the
+ * entropy's, which uses the fp32 base-2 logarithm); workgroup reductions run
+ * in a fixed order.
+ *
+ * mxattn_softmax_rows materializes p = softmax(q k^T / sqrt(d)) for the query
+ * rows [row0, row0 + rows) of every (batch, head): S on the bf16 matrix cores
+ * with fp32 accumulation, p = 2^(s log2(e)/sqrt(d) - m) / L in fp32 (entries
+ * below 2^-126 flush to 0).
+ *   q       device bf16 [B, H, Nq, d]; k device bf16 [B, H, Nkv, d]
+ *   p       device fp32 [B, H, rows, ld], ld >= Nkv, ld % 4 == 0; entries
+ *           past Nkv up to the next multiple of 4 are set to 0, the rest of
+ *           [Nkv, ld) is not written
+ * mxattn_rowsum_diag quantizes given rows:
+ *   p       device fp32 [rows, ld], entries >= 0 (first N of each row used),
+ *           ld >= N, ld % 4 == 0, 16-byte aligned
+ *   stats   device fp64 [rows, 8]
+ * mxattn_attention_rowsum_diag computes the same statistics for every query
+ * row of q against k without materializing P: the probabilities are formed
+ * exactly as mxattn_softmax_rows forms them and quantized in registers, so
+ * the result equals mxattn_rowsum_diag applied to mxattn_softmax_rows up to
+ * the order of the fp64 additions.  No workspace.
+ *   stats   device fp64 [B, H, Nq, 8]
+ * All three return MXATTN_OK or an error status; nothing is launched on
+ * error. */
+int mxattn_softmax_rows(const void* q, const void* k, float* p, int64_t B, int64_t H, int64_t Nq,
+                        int64_t Nkv, int64_t d, int64_t row0, int64_t rows, int64_t ld, void* stream);
+int mxattn_rowsum_diag(const float* p, int64_t rows, int64_t N, int64_t ld, int mode, float gamma,
+                       double* stats, void* stream);
+int mxattn_attention_rowsum_diag(const void* q, const void* k, int64_t B, int64_t H, int64_t Nq,
+                                 int64_t Nkv, int64_t d, int mode, float gamma, double* stats,
+                                 void* stream);
 
 /* MXFP4 attention forward O = softmax(Q K^T / sqrt(d)) V with MXFP4 Q, K, V
  * and MXFP4 P~ (Algorithm 2, with its Hadamard rotation in mode

@@ -13,7 +13,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libmxattn.so")
-SOURCES = ["api.hip", "quantize.hip", "attention.hip", "qmax.hip"]
+SOURCES = ["api.hip", "quantize.hip", "attention.hip", "qmax.hip", "rowsum.hip"]
 ARCH = "gfx950"
 
 

@@ -78,7 +78,7 @@ const char* mxattn_status_string(int s) {
         case MXATTN_ERR_UNSUPPORTED: return "unsupported head dimension (d must be 128)";
         case MXATTN_ERR_OOM: return "workspace allocation failed";
         case MXATTN_ERR_HIP: return "HIP runtime error";
-        case MXATTN_ERR_BOUNDARY: return "invalid scale boundary (need 4 <= q <= 8 and 1 <= nq <= 64)";
+        case MXATTN_ERR_BOUNDARY: return "invalid scale boundary (need 4 <= q <= 8 and 1 <= nq <= 64) or pre-scale (need 0 < gamma < 3e38)";
         default: return "unknown status";
     }
 }
@@ -168,6 +168,90 @@ int mxattn_qmax_sse(const void* x, int block_axis, const double* qs, int nq, dou
         st = MXATTN_ERR_HIP;
     }
     return st;
+}
+
+int mxattn_softmax_rows(const void* q, const void* k, float* p, int64_t B, int64_t H, int64_t Nq,
+                        int64_t Nkv, int64_t d, int64_t row0, int64_t rows, int64_t ld, void* stream) {
+    if (!q || !k || !p) return MXATTN_ERR_NULL;
+    if (int st = check_shape(B, H, Nq, d)) return st;
+    if (int st = check_shape(B, H, Nkv, d)) return st;
+    if (row0 < 0 || rows < 1 || row0 + rows > Nq || ld < Nkv || ld % 4 != 0 || ld > (1 << 28))
+        return MXATTN_ERR_SHAPE;
+    const int64_t qtiles = (rows + 127) / 128;
+    if (B * H * qtiles > ((int64_t)1 << 31) - 1) return MXATTN_ERR_SHAPE;
+    if (!aligned(q, 16) || !aligned(k, 16) || !aligned(p, 16)) return MXATTN_ERR_ALIGN;
+    mxattn::SoftmaxRowsArgs a{};
+    a.q = static_cast<const uint16_t*>(q);
+    a.k = static_cast<const uint16_t*>(k);
+    a.p = p;
+    a.Nq = (int)Nq;
+    a.Nkv = (int)Nkv;
+    a.row0 = (int)row0;
+    a.rows = (int)rows;
+    a.ld = (int)ld;
+    hipError_t e = mxattn::launch_attn_rows(a, B * H, mxattn::kRowsStoreP, reinterpret_cast<hipStream_t>(stream));
+    if (e != hipSuccess) {
+        set_error("softmax rows launch", e);
+        return MXATTN_ERR_HIP;
+    }
+    return MXATTN_OK;
+}
+
+static bool valid_gamma(float gamma) { return gamma > 0.0f && gamma < 3.0e38f; }
+
+int mxattn_rowsum_diag(const float* p, int64_t rows, int64_t N, int64_t ld, int mode, float gamma,
+                       double* stats, void* stream) {
+    if (!p || !stats) return MXATTN_ERR_NULL;
+    if (!valid_mode(mode)) return MXATTN_ERR_MODE;
+    if (rows < 1 || rows > ((int64_t)1 << 31) - 1 || N < 1 || N > (1 << 28) || ld < N || ld % 4 != 0)
+        return MXATTN_ERR_SHAPE;
+    if (!valid_gamma(gamma)) return MXATTN_ERR_BOUNDARY;
+    if (!aligned(p, 16) || !aligned(stats, 8)) return MXATTN_ERR_ALIGN;
+    mxattn::RowsumDiagArgs a{};
+    a.p = p;
+    a.N = N;
+    a.ld = ld;
+    a.gamma = gamma;
+    a.g = 1.0 / (double)gamma;
+    a.stats = stats;
+    a.rows_per_head = rows;
+    a.out_rows_per_head = rows;
+    a.out_row0 = 0;
+    hipError_t e = mxattn::launch_rowsum_diag(a, rows, rule_of(mode), reinterpret_cast<hipStream_t>(stream));
+    if (e != hipSuccess) {
+        set_error("row-sum diagnostic launch", e);
+        return MXATTN_ERR_HIP;
+    }
+    return MXATTN_OK;
+}
+
+int mxattn_attention_rowsum_diag(const void* q, const void* k, int64_t B, int64_t H, int64_t Nq,
+                                 int64_t Nkv, int64_t d, int mode, float gamma, double* stats,
+                                 void* stream) {
+    if (!q || !k || !stats) return MXATTN_ERR_NULL;
+    if (!valid_mode(mode)) return MXATTN_ERR_MODE;
+    if (int st = check_shape(B, H, Nq, d)) return st;
+    if (int st = check_shape(B, H, Nkv, d)) return st;
+    if (!valid_gamma(gamma)) return MXATTN_ERR_BOUNDARY;
+    if (!aligned(q, 16) || !aligned(k, 16) || !aligned(stats, 8)) return MXATTN_ERR_ALIGN;
+    if (B * H * ((Nq + 127) / 128) > ((int64_t)1 << 31) - 1) return MXATTN_ERR_SHAPE;
+    mxattn::SoftmaxRowsArgs a{};
+    a.q = static_cast<const uint16_t*>(q);
+    a.k = static_cast<const uint16_t*>(k);
+    a.Nq = (int)Nq;
+    a.Nkv = (int)Nkv;
+    a.row0 = 0;
+    a.rows = (int)Nq;
+    a.gamma = gamma;
+    a.g = 1.0 / (double)gamma;
+    a.stats = stats;
+    const int out = rule_of(mode) == mxattn::kRuleUos ? mxattn::kRowsDiagUos : mxattn::kRowsDiagOcp;
+    hipError_t e = mxattn::launch_attn_rows(a, B * H, out, reinterpret_cast<hipStream_t>(stream));
+    if (e != hipSuccess) {
+        set_error("row-sum diagnostic launch", e);
+        return MXATTN_ERR_HIP;
+    }
+    return MXATTN_OK;
 }
 
 // Rearranges the K^/V^ scales into sc (mxattn::tile_scales_bytes(B*H, Nkv)

@@ -57,6 +57,35 @@ inline int64_t tile_scales_bytes(int64_t BH, int64_t N) { return BH * ((N + 127)
 hipError_t launch_tile_scales(const uint8_t* ks, const uint8_t* vs, uint8_t* out, int64_t BH, int64_t N,
                               hipStream_t stream);
 
+// Row-sum diagnostics (rowsum.hip).  Attention rows [row0, row0 + rows) of
+// every head: either p [BH, rows, ld] fp32 stored, or their quantization
+// statistics written to stats [BH, Nq, 8] (fp64).
+enum RowsOut { kRowsStoreP = 0, kRowsDiagUos = 1, kRowsDiagOcp = 2 };
+struct SoftmaxRowsArgs {
+    const uint16_t* q;  // [BH, Nq, 128] bf16
+    const uint16_t* k;  // [BH, Nkv, 128] bf16
+    float* p;           // [BH, rows, ld] (kRowsStoreP)
+    int Nq, Nkv, row0, rows, ld;
+    float gamma;        // pre-scale (diagnostics)
+    double g;           // fp64(1 / gamma)
+    double* stats;      // [BH, Nq, 8] (diagnostics)
+    int qtiles;         // set by the launcher
+    float c;            // set by the launcher: log2(e) / sqrt(128)
+};
+hipError_t launch_attn_rows(const SoftmaxRowsArgs& a, int64_t BH, int out, hipStream_t stream);
+
+// Diagnostics of rows of p [n_rows, ld] (first N entries), written to
+// stats[((r / rows_per_head) * out_rows_per_head + out_row0 + r % rows_per_head) * 8 + i].
+struct RowsumDiagArgs {
+    const float* p;
+    int64_t N, ld;
+    float gamma;  // pre-scale
+    double g;     // fp64(1 / gamma)
+    double* stats;
+    int64_t rows_per_head, out_rows_per_head, out_row0;
+};
+hipError_t launch_rowsum_diag(const RowsumDiagArgs& a, int64_t n_rows, int rule, hipStream_t stream);
+
 // mode: 0 OCP + direct, 1 UOS + direct, 2 UOS + PNQ
 hipError_t launch_attention(const AttnArgs& a, int mode, hipStream_t stream);
 

@@ -50,6 +50,13 @@ def lib() -> ctypes.CDLL:
             L.mxattn_quantize_qmax.restype = I
             L.mxattn_qmax_sse.argtypes = [P, I, P, I, P, I64, I64, I64, I64, P]
             L.mxattn_qmax_sse.restype = I
+            F = ctypes.c_float
+            L.mxattn_softmax_rows.argtypes = [P, P, P, I64, I64, I64, I64, I64, I64, I64, I64, P]
+            L.mxattn_softmax_rows.restype = I
+            L.mxattn_rowsum_diag.argtypes = [P, I64, I64, I64, I, F, P, P]
+            L.mxattn_rowsum_diag.restype = I
+            L.mxattn_attention_rowsum_diag.argtypes = [P, P, I64, I64, I64, I64, I64, I, F, P, P]
+            L.mxattn_attention_rowsum_diag.restype = I
             L.mxattn_forward.argtypes = [P, P, P, P, I64, I64, I64, I64, I, P]
             L.mxattn_forward.restype = I
             L.mxattn_attend.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I, P]
@@ -153,6 +160,58 @@ def qmax_sse(x: torch.Tensor, block_axis: int, qs, stream=None, out=None):
     st = lib().mxattn_qmax_sse(x.data_ptr(), block_axis, ctypes.cast(q, ctypes.c_void_p), len(qs),
                                out.data_ptr(), B, H, N, d, _stream(stream))
     _check(st, "mxattn_qmax_sse")
+    return out
+
+
+DIAG_FIELDS = ("rowsum", "mass", "zeroing", "saturation", "down", "up", "exact", "entropy")
+
+
+def softmax_rows(q: torch.Tensor, k: torch.Tensor, row0: int = 0, rows: int | None = None, ld=None,
+                 stream=None, out=None):
+    """fp32 softmax(q k^T / sqrt(d)) for query rows [row0, row0 + rows) of
+    every head: [B, H, rows, ld] (ld = Nkv rounded up to 4; entries past Nkv
+    are left as allocated)."""
+    B, H, Nq, d = _bhnd(q)
+    Bk, Hk, Nkv, dk = _bhnd(k)
+    if (Bk, Hk, dk) != (B, H, d):
+        raise ValueError("k must be [B, H, Nkv, d] with q's B, H, d")
+    rows = Nq - row0 if rows is None else rows
+    ld = (Nkv + 3) // 4 * 4 if ld is None else ld
+    if out is None:
+        out = torch.empty((B, H, rows, ld), dtype=torch.float32, device=q.device)
+    st = lib().mxattn_softmax_rows(q.data_ptr(), k.data_ptr(), out.data_ptr(), B, H, Nq, Nkv, d, row0,
+                                   rows, ld, _stream(stream))
+    _check(st, "mxattn_softmax_rows")
+    return out
+
+
+def rowsum_diag(p: torch.Tensor, N: int, mode, gamma: float = 1.0, stream=None, out=None):
+    """Row-sum diagnostics of fp32 rows p [..., ld] (first N entries): [rows, 8]
+    float64 in DIAG_FIELDS order."""
+    if p.dtype != torch.float32 or not p.is_cuda or not p.is_contiguous():
+        raise ValueError("expected a contiguous fp32 CUDA tensor")
+    ld = p.shape[-1]
+    rows = p.numel() // ld
+    if out is None:
+        out = torch.empty((rows, 8), dtype=torch.float64, device=p.device)
+    st = lib().mxattn_rowsum_diag(p.data_ptr(), rows, N, ld, _mode(mode), float(gamma), out.data_ptr(),
+                                  _stream(stream))
+    _check(st, "mxattn_rowsum_diag")
+    return out
+
+
+def attention_rowsum_diag(q: torch.Tensor, k: torch.Tensor, mode, gamma: float = 1.0, stream=None,
+                          out=None):
+    """Row-sum diagnostics of every attention row: [B, H, Nq, 8] float64."""
+    B, H, Nq, d = _bhnd(q)
+    Bk, Hk, Nkv, dk = _bhnd(k)
+    if (Bk, Hk, dk) != (B, H, d):
+        raise ValueError("k must be [B, H, Nkv, d] with q's B, H, d")
+    if out is None:
+        out = torch.empty((B, H, Nq, 8), dtype=torch.float64, device=q.device)
+    st = lib().mxattn_attention_rowsum_diag(q.data_ptr(), k.data_ptr(), B, H, Nq, Nkv, d, _mode(mode),
+                                            float(gamma), out.data_ptr(), _stream(stream))
+    _check(st, "mxattn_attention_rowsum_diag")
     return out
 
 

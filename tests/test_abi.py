@@ -132,3 +132,28 @@ def test_boundary_entry_points_reject_bad_arguments(L):
     assert s(FAKE, 2, bad, 3, FAKE, 1, 1, 8, 128, None) == 9
     assert s(FAKE, 3, qs, 64, FAKE + 4, 1, 1, 8, 128, None) == 3       # sse needs 8 bytes
     assert s(FAKE, 3, qs, 64, FAKE, 1, 1, 8, 96, None) == 6
+
+
+def test_rowsum_entry_points_reject_bad_arguments(L):
+    s = L.mxattn_softmax_rows
+    assert s(None, FAKE, FAKE, 1, 1, 8, 8, 128, 0, 8, 8, None) == 1
+    assert s(FAKE, FAKE, FAKE, 1, 1, 8, 8, 128, 4, 5, 8, None) == 2     # rows past Nq
+    assert s(FAKE, FAKE, FAKE, 1, 1, 8, 8, 128, 0, 0, 8, None) == 2     # no rows
+    assert s(FAKE, FAKE, FAKE, 1, 1, 8, 8, 128, 0, 8, 6, None) == 2     # ld < Nkv
+    assert s(FAKE, FAKE, FAKE, 1, 1, 8, 10, 128, 0, 8, 10, None) == 2   # ld % 4
+    assert s(FAKE, FAKE, FAKE, 1, 1, 8, 8, 64, 0, 8, 8, None) == 6
+    assert s(FAKE, FAKE, FAKE + 4, 1, 1, 8, 8, 128, 0, 8, 8, None) == 3
+    d = L.mxattn_rowsum_diag
+    assert d(None, 4, 8, 8, 1, 1.0, FAKE, None) == 1
+    assert d(FAKE, 4, 8, 8, 9, 1.0, FAKE, None) == 4
+    assert d(FAKE, 0, 8, 8, 1, 1.0, FAKE, None) == 2
+    assert d(FAKE, 4, 9, 8, 1, 1.0, FAKE, None) == 2                     # ld < N
+    assert d(FAKE, 4, 8, 8, 1, 0.0, FAKE, None) == 9                     # gamma
+    assert d(FAKE, 4, 8, 8, 1, float("nan"), FAKE, None) == 9
+    assert d(FAKE + 8, 4, 8, 8, 1, 1.0, FAKE, None) == 3
+    assert d(FAKE, 4, 8, 8, 1, 1.0, FAKE + 4, None) == 3
+    a = L.mxattn_attention_rowsum_diag
+    assert a(FAKE, FAKE, 1, 1, 8, 8, 128, 1, 1.0, None, None) == 1
+    assert a(FAKE, FAKE, 1, 1, 0, 8, 128, 1, 1.0, FAKE, None) == 2
+    assert a(FAKE, FAKE, 1, 1, 8, 8, 128, 7, 1.0, FAKE, None) == 4
+    assert a(FAKE, FAKE, 1, 1, 8, 8, 128, 1, -1.0, FAKE, None) == 9
