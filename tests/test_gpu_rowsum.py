@@ -206,3 +206,25 @@ def test_report_rowsum_statistics(mx):
                 f"{100 * (st[hi, 0] < 1).mean() if hi.any() else float('nan'):.1f}%")
             assert np.allclose(st[:, 0] - st[:, 1], st[:, 2:7].sum(axis=1), atol=1e-12)
         torch.cuda.empty_cache()
+
+
+def test_report_global_prescale(mx):
+    """Fig. pnq_rowsum (C): one pre-quantization factor gamma for the whole
+    tensor.  With power-of-two shared scales only the fraction of log2 gamma
+    matters, so gamma runs over one octave (logged)."""
+    for cfg in (1, 2):
+        w = inputs.workload(cfg)
+        q, k, _ = workload_bits(cfg)
+        qt, kt = mx.bf16_from_bits(q), mx.bf16_from_bits(k)
+        for mode in MODES:
+            parts = []
+            for i in range(8):
+                gamma = 2.0 ** (i / 8)
+                st = mx.attention_rowsum_diag(qt, kt, mode, gamma).cpu().numpy().reshape(-1, 8)
+                parts.append(f"{gamma:.3f}: {st[:, 0].mean():.4f}/{100 * (st[:, 0] > 1).mean():.0f}%")
+                if i == 0:  # gamma = 2 quantizes the same values (subnormal p aside)
+                    np.testing.assert_allclose(
+                        st, mx.attention_rowsum_diag(qt, kt, mode, 2.0).cpu().numpy().reshape(-1, 8),
+                        rtol=0, atol=1e-20)
+            log(f"[rowsum prescale] {w.name} {mode} (gamma: mean row sum / rows above 1): " + ", ".join(parts))
+        torch.cuda.empty_cache()
