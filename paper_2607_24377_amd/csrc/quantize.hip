@@ -133,11 +133,12 @@ __global__ __launch_bounds__(256) void quantize_headdim_rot_kernel(const uint4* 
 // ---------------------------------------------------------------------------
 // Blocks along the token axis (V).  A workgroup stages 128 tokens x 128
 // channels of one head (32 KiB of bf16) in LDS with coalesced 16-byte loads;
-// wave w then quantizes token block w of the group, each lane owning a pair
-// of channels.  Tokens past N are staged as +0 (the zero padding of the last
-// block).  Output rows are tokens-contiguous per channel: 16 code bytes and
-// one scale byte per (channel, 32-token block).
-// ---------------------------------------------------------------------------
+// tokens past N are staged as +0 (the zero padding of the last block).  Wave w
+// then quantizes channel pairs 16w..16w+15 over the group's four 32-token
+// blocks, lane (pair p, block b) owning one block of two channels.  Output
+// rows are tokens-contiguous per channel (16 code bytes and one scale byte per
+// (channel, 32-token block)), so the four lanes of a pair write the pair's 64
+// code bytes of this group contiguously.
 constexpr int kVqTokens = 128;
 
 template <int kRule>
@@ -145,7 +146,10 @@ __global__ __launch_bounds__(256) void quantize_tokens_kernel(const uint4* __res
                                                               uint8_t* __restrict__ codes,
                                                               uint8_t* __restrict__ scales, int N,
                                                               int nb, int groups, Boundary bq) {
-    __shared__ uint32_t tile[kVqTokens * 64];  // [token][64 dwords = 128 bf16]
+    // [token][64 dwords = 128 bf16]; the 32-token quarter q of the group is
+    // stored with its dword columns XOR-ed by 16 q, so that the four lanes
+    // reading the same channel pair in four quarters hit four bank groups
+    __shared__ uint32_t tile[kVqTokens * 64];
     const int tid = threadIdx.x;
     const int bh = blockIdx.x / groups;
     const int g = blockIdx.x % groups;
@@ -158,20 +162,24 @@ __global__ __launch_bounds__(256) void quantize_tokens_kernel(const uint4* __res
         int tok = ch >> 4, part = ch & 15;
         uint4 v = make_uint4(0, 0, 0, 0);
         if (tok0 + tok < N) v = src[(int64_t)(tok0 + tok) * 16 + part];
-        *reinterpret_cast<uint4*>(&tile[tok * 64 + part * 4]) = v;
+        *reinterpret_cast<uint4*>(&tile[tok * 64 + ((part * 4) ^ (16 * (tok >> 5)))]) = v;
     }
     __syncthreads();
 
-    const int w = tid >> 6;   // token block within the group
-    const int cp = tid & 63;  // channels 2cp, 2cp+1
-    const int blk = 4 * g + w;
+    // wave w: channel pairs 16 w .. 16 w + 15; lane: pair p = lane / 4, token
+    // block b = lane % 4 of the group.  The four lanes of a pair write the
+    // pair's four 16-byte code chunks of this group next to each other.
+    const int w = tid >> 6, lane = tid & 63;
+    const int p = lane >> 2, b = lane & 3;
+    const int cp = 16 * w + p;  // channels 2cp, 2cp+1 (dword column cp)
+    const int blk = 4 * g + b;
     if (blk >= nb) return;
 
     uint32_t col[32];
     uint32_t m0 = 0, m1 = 0;
 #pragma unroll
     for (int t = 0; t < 32; t++) {
-        uint32_t d = tile[(32 * w + t) * 64 + cp];
+        uint32_t d = tile[(32 * b + t) * 64 + (cp ^ (16 * b))];
         col[t] = d;
         m0 = max(m0, d & 0x7FFFu);
         m1 = max(m1, (d >> 16) & 0x7FFFu);
