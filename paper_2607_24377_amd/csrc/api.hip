@@ -278,8 +278,17 @@ static int launch_attend(const uint8_t* qc, const uint8_t* qs, const uint8_t* kc
     a.Nq = (int)Nq;
     a.nb = (int)((Nkv + 31) / 32);
     a.qtiles = (int)((Nq + mxattn::kQueryTile - 1) / mxattn::kQueryTile);
-    const int64_t total = B * H * a.qtiles;
-    if (total > (int64_t)1 << 30) return MXATTN_ERR_SHAPE;
+    if (B * H * a.qtiles > (int64_t)1 << 30) return MXATTN_ERR_SHAPE;
+    // one query tile per workgroup; with K^/V^ resident in LDS, as many as
+    // keep about 1024 workgroups (4 per CU) busy, at most 16
+    int64_t qpw = 1;
+    if (Nkv <= mxattn::kResidentKeys) {
+        qpw = B * H * a.qtiles / 1024;
+        qpw = qpw < 1 ? 1 : (qpw > 16 ? 16 : qpw);
+    }
+    a.qt_per_wg = (int)qpw;
+    a.nchunks = (int)((a.qtiles + qpw - 1) / qpw);
+    const int64_t total = B * H * a.nchunks;
     a.total_tiles = (int)total;
     a.per_xcd = (int)((total + 7) / 8);
     e = mxattn::launch_attention(a, kernel_mode(mode), s);

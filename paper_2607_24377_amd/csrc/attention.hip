@@ -172,6 +172,201 @@ __device__ __forceinline__ uint32_t cvt_fp4x2(uint32_t old, float a, float b, fl
     }
 }
 
+// One KV tile of Algorithm 2 for the wave's 32 query rows, on the tile's
+// stage in LDS: S^T = K^ Q^T, the online-softmax update of (m, l), P^ and
+// O~^T += V^T P^T.  Reads LDS only; the caller owns loads and barriers.
+template <int kRule, bool kPnq>
+__device__ __forceinline__ void attend_tile(const uint8_t* st, int tile, int N, int q, int h, int lane,
+                                            const v8i& qB0, const v8i& qB1, int qS0, int qS1,
+                                            const v8i& ones, float& m, float& lacc, v16f (&O)[4]) {
+    const float cl = 0.12751743082459868f;  // fp32(log2(e) / sqrt(128))
+    uint2 ksb = lds_read64(lds_addr(st + kKsOff + lane * 8));
+    uint2 vsb = lds_read64(lds_addr(st + kVsOff + lane * 8));
+
+    // ---- K^ operands for the 8 S products (chunk c, tile j, half hf)
+    v4i kr[2][2][2];
+#pragma unroll
+    for (int c = 0; c < 2; c++)
+#pragma unroll
+        for (int j = 0; j < 2; j++) {
+            const int row = 64 * c + 32 * j + q;
+            const uint8_t* rp = st + kKcOff + row * 64;
+            const int sw = swz(row);
+            kr[c][j][0] = lds_read128(lds_addr(rp + 16 * ((0 + h) ^ sw)));
+            kr[c][j][1] = lds_read128(lds_addr(rp + 16 * ((2 + h) ^ sw)));
+        }
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(kr[0][0][0]), "+v"(kr[0][0][1]), "+v"(kr[0][1][0]), "+v"(kr[0][1][1]),
+                   "+v"(kr[1][0][0]), "+v"(kr[1][0][1]), "+v"(kr[1][1][0]), "+v"(kr[1][1][1]), "+v"(ksb),
+                   "+v"(vsb));
+    v8i kop[2][2][2];
+#pragma unroll
+    for (int c = 0; c < 2; c++)
+#pragma unroll
+        for (int j = 0; j < 2; j++) {
+            kop[c][j][0] = fp4_v(kr[c][j][0]);
+            kop[c][j][1] = fp4_v(kr[c][j][1]);
+        }
+
+    // ---- S^T = K^ Q^T: S[c][j][i] is key 64c + 32h + 16j + i of the tile
+    v16f S[2][2];
+#pragma unroll
+    for (int c = 0; c < 2; c++) {
+        const int sreg = c == 0 ? (int)ksb.x : (int)ksb.y;
+#pragma unroll
+        for (int j = 0; j < 2; j++) {
+            v16f acc;
+#pragma unroll
+            for (int i = 0; i < 16; i++) acc[i] = 0.f;
+            if (j == 0) {
+                acc = mfma_fp4<0>(kop[c][j][0], qB0, acc, sreg, qS0);
+                acc = mfma_fp4<1>(kop[c][j][1], qB1, acc, sreg, qS1);
+            } else {
+                acc = mfma_fp4<2>(kop[c][j][0], qB0, acc, sreg, qS0);
+                acc = mfma_fp4<3>(kop[c][j][1], qB1, acc, sreg, qS1);
+            }
+            S[c][j] = acc;
+        }
+    }
+
+    // ---- V^ operands for the PV products (read now, used after softmax)
+    v4i vr[4][2];
+#pragma unroll
+    for (int n = 0; n < 4; n++) {
+        const int row = 32 * n + q;
+        const uint8_t* rp = st + kVcOff + row * 64;
+        const int sw = swz(row);
+        vr[n][0] = lds_read128(lds_addr(rp + 16 * ((0 + h) ^ sw)));
+        vr[n][1] = lds_read128(lds_addr(rp + 16 * ((2 + h) ^ sw)));
+    }
+
+    // ---- mask keys past the end of the sequence (last tile only)
+    const int k0 = tile * 128;
+    if (k0 + 128 > N) {
+#pragma unroll
+        for (int c = 0; c < 2; c++)
+#pragma unroll
+            for (int j = 0; j < 2; j++)
+#pragma unroll
+                for (int i = 0; i < 16; i++)
+                    if (k0 + 64 * c + 32 * h + 16 * j + i >= N) S[c][j][i] = -__builtin_inff();
+    }
+
+    // ---- running maximum
+    float bmax[2];
+#pragma unroll
+    for (int c = 0; c < 2; c++) {
+        float mx = S[c][0][0];
+#pragma unroll
+        for (int j = 0; j < 2; j++)
+#pragma unroll
+            for (int i = 0; i < 16; i++) mx = fmaxf(mx, S[c][j][i]);
+        bmax[c] = mx;
+    }
+    float rmax = fmaxf(bmax[0], bmax[1]);
+    rmax = max_with_other_half(rmax);
+    float u = cl * rmax;
+    if (__builtin_fmaf(rmax, cl, -u) < 0.f) u = next_down(u);  // RD(c * max s)
+    const float m_new = fmaxf(m, u);
+    const float alpha = __builtin_amdgcn_exp2f(m - m_new);  // 0 on the first tile
+    m = m_new;
+
+    // ---- P~, its MXFP4 quantization P^, row-sum contribution
+    v8i P[2];
+    int psc[2];
+    float lsum = 0.f;
+#pragma unroll
+    for (int c = 0; c < 2; c++) {
+        const float mb = __builtin_amdgcn_exp2f(__builtin_fmaf(bmax[c], cl, -m_new));
+        const uint32_t mbits = __builtin_bit_cast(uint32_t, mb);
+        const uint32_t sbyte =
+            (mbits < 0x00800000u) ? 127u : (uint32_t)(scale_exponent_f32<kRule>(mbits) + 127);
+        const float sf = e8m0_as_f32(sbyte);
+        psc[c] = (int)sbyte;
+        uint32_t w[4] = {0, 0, 0, 0};
+#pragma unroll
+        for (int n = 0; n < 32; n += 2) {
+            const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(S[c][n >> 4][n & 15], cl, -m_new));
+            const float p1 =
+                __builtin_amdgcn_exp2f(__builtin_fmaf(S[c][(n + 1) >> 4][(n + 1) & 15], cl, -m_new));
+            if (!kPnq) lsum += p0 + p1;
+            w[n >> 3] = cvt_fp4x2(w[n >> 3], p0, p1, sf, (n & 7) >> 1);
+        }
+        P[c] = fp4_operand(make_uint4(w[0], w[1], w[2], w[3]));
+    }
+
+    float dl;
+    if (kPnq) {
+        v16f lt;
+#pragma unroll
+        for (int i = 0; i < 16; i++) lt[i] = 0.f;
+        lt = mfma_fp4<0>(ones, P[0], lt, 127, psc[0]);
+        lt = mfma_fp4<0>(ones, P[1], lt, 127, psc[1]);
+        dl = lt[0];
+    } else {
+        dl = lsum;  // this lane's half of the row; halves are added at the end
+    }
+    lacc = alpha * lacc + dl;
+
+    // ---- O~^T = diag(alpha) O~^T + V^T P^T
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(vr[0][0]), "+v"(vr[0][1]), "+v"(vr[1][0]), "+v"(vr[1][1]), "+v"(vr[2][0]),
+                   "+v"(vr[2][1]), "+v"(vr[3][0]), "+v"(vr[3][1]));
+    v8i vop[4][2];
+#pragma unroll
+    for (int n = 0; n < 4; n++) {
+        vop[n][0] = fp4_v(vr[n][0]);
+        vop[n][1] = fp4_v(vr[n][1]);
+    }
+    if (__any(alpha != 1.f)) {
+#pragma unroll
+        for (int n = 0; n < 4; n++)
+#pragma unroll
+            for (int i = 0; i < 16; i++) O[n][i] *= alpha;
+    }
+#pragma unroll
+    for (int n = 0; n < 4; n++) {
+        const int sreg = n < 2 ? (int)vsb.x : (int)vsb.y;
+        // scale byte index 2n + c within the lane's 8 bytes
+        if ((n & 1) == 0) {
+            O[n] = mfma_fp4<0>(vop[n][0], P[0], O[n], sreg, psc[0]);
+            O[n] = mfma_fp4<1>(vop[n][1], P[1], O[n], sreg, psc[1]);
+        } else {
+            O[n] = mfma_fp4<2>(vop[n][0], P[0], O[n], sreg, psc[0]);
+            O[n] = mfma_fp4<3>(vop[n][1], P[1], O[n], sreg, psc[1]);
+        }
+    }
+
+}
+
+// O = O~ / l rounded to bf16 (Eq. online_attention_output), as O~ times the
+// fp32 reciprocal of l; lane (q, h) holds channels 32 n + 8 g + 4 h + (0..3)
+// of its query row.
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+template <bool kPnq>
+__device__ __forceinline__ void store_rows(const AttnArgs& a, int64_t rowbase, int qi, int h, float lacc,
+                                           const v16f (&O)[4]) {
+    float ltot = lacc;
+    if (!kPnq) ltot += __shfl_xor(lacc, 32);
+    const float inv = 1.0f / ltot;  // one division, then 64 products
+    if (qi < a.Nq) {
+        uint16_t* orow = a.out + (int64_t)(rowbase + qi) * 128;
+#pragma unroll
+        for (int n = 0; n < 4; n++) {
+#pragma unroll
+            for (int g = 0; g < 4; g++) {
+                // round to nearest even with the packed hardware conversion
+                const f32x2 lo = {O[n][4 * g + 0] * inv, O[n][4 * g + 1] * inv};
+                const f32x2 hi = {O[n][4 * g + 2] * inv, O[n][4 * g + 3] * inv};
+                *reinterpret_cast<uint2*>(orow + 32 * n + 8 * g + 4 * h) =
+                    make_uint2(__builtin_bit_cast(uint32_t, __builtin_convertvector(lo, bf16x2)),
+                               __builtin_bit_cast(uint32_t, __builtin_convertvector(hi, bf16x2)));
+            }
+        }
+    }
+}
+
 template <int kRule, bool kPnq>
 __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
     __shared__ __attribute__((aligned(16))) uint8_t lds[2 * kStageBytes];
@@ -211,7 +406,6 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < 8; i++) ones[i] = i < 4 ? 0x22222222 : 0;
 
-    const float cl = 0.12751743082459868f;  // fp32(log2(e) / sqrt(128))
     float m = -__builtin_inff();
     float lacc = 0.f;
     v16f O[4];
@@ -231,184 +425,90 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
             load_tile_scales(next, a, bh, tile + 1, wave, lane);
         }
 
-        uint2 ksb = lds_read64(lds_addr(st + kKsOff + lane * 8));
-        uint2 vsb = lds_read64(lds_addr(st + kVsOff + lane * 8));
-
-        // ---- K^ operands for the 8 S products (chunk c, tile j, half hf)
-        v4i kr[2][2][2];
-#pragma unroll
-        for (int c = 0; c < 2; c++)
-#pragma unroll
-            for (int j = 0; j < 2; j++) {
-                const int row = 64 * c + 32 * j + q;
-                const uint8_t* rp = st + kKcOff + row * 64;
-                const int sw = swz(row);
-                kr[c][j][0] = lds_read128(lds_addr(rp + 16 * ((0 + h) ^ sw)));
-                kr[c][j][1] = lds_read128(lds_addr(rp + 16 * ((2 + h) ^ sw)));
-            }
-        asm volatile("s_waitcnt lgkmcnt(0)"
-                     : "+v"(kr[0][0][0]), "+v"(kr[0][0][1]), "+v"(kr[0][1][0]), "+v"(kr[0][1][1]),
-                       "+v"(kr[1][0][0]), "+v"(kr[1][0][1]), "+v"(kr[1][1][0]), "+v"(kr[1][1][1]), "+v"(ksb),
-                       "+v"(vsb));
-        v8i kop[2][2][2];
-#pragma unroll
-        for (int c = 0; c < 2; c++)
-#pragma unroll
-            for (int j = 0; j < 2; j++) {
-                kop[c][j][0] = fp4_v(kr[c][j][0]);
-                kop[c][j][1] = fp4_v(kr[c][j][1]);
-            }
-
-        // ---- S^T = K^ Q^T: S[c][j][i] is key 64c + 32h + 16j + i of the tile
-        v16f S[2][2];
-#pragma unroll
-        for (int c = 0; c < 2; c++) {
-            const int sreg = c == 0 ? (int)ksb.x : (int)ksb.y;
-#pragma unroll
-            for (int j = 0; j < 2; j++) {
-                v16f acc;
-#pragma unroll
-                for (int i = 0; i < 16; i++) acc[i] = 0.f;
-                if (j == 0) {
-                    acc = mfma_fp4<0>(kop[c][j][0], qB0, acc, sreg, qS0);
-                    acc = mfma_fp4<1>(kop[c][j][1], qB1, acc, sreg, qS1);
-                } else {
-                    acc = mfma_fp4<2>(kop[c][j][0], qB0, acc, sreg, qS0);
-                    acc = mfma_fp4<3>(kop[c][j][1], qB1, acc, sreg, qS1);
-                }
-                S[c][j] = acc;
-            }
-        }
-
-        // ---- V^ operands for the PV products (read now, used after softmax)
-        v4i vr[4][2];
-#pragma unroll
-        for (int n = 0; n < 4; n++) {
-            const int row = 32 * n + q;
-            const uint8_t* rp = st + kVcOff + row * 64;
-            const int sw = swz(row);
-            vr[n][0] = lds_read128(lds_addr(rp + 16 * ((0 + h) ^ sw)));
-            vr[n][1] = lds_read128(lds_addr(rp + 16 * ((2 + h) ^ sw)));
-        }
-
-        // ---- mask keys past the end of the sequence (last tile only)
-        const int k0 = tile * 128;
-        if (k0 + 128 > N) {
-#pragma unroll
-            for (int c = 0; c < 2; c++)
-#pragma unroll
-                for (int j = 0; j < 2; j++)
-#pragma unroll
-                    for (int i = 0; i < 16; i++)
-                        if (k0 + 64 * c + 32 * h + 16 * j + i >= N) S[c][j][i] = -__builtin_inff();
-        }
-
-        // ---- running maximum
-        float bmax[2];
-#pragma unroll
-        for (int c = 0; c < 2; c++) {
-            float mx = S[c][0][0];
-#pragma unroll
-            for (int j = 0; j < 2; j++)
-#pragma unroll
-                for (int i = 0; i < 16; i++) mx = fmaxf(mx, S[c][j][i]);
-            bmax[c] = mx;
-        }
-        float rmax = fmaxf(bmax[0], bmax[1]);
-        rmax = max_with_other_half(rmax);
-        float u = cl * rmax;
-        if (__builtin_fmaf(rmax, cl, -u) < 0.f) u = next_down(u);  // RD(c * max s)
-        const float m_new = fmaxf(m, u);
-        const float alpha = __builtin_amdgcn_exp2f(m - m_new);  // 0 on the first tile
-        m = m_new;
-
-        // ---- P~, its MXFP4 quantization P^, row-sum contribution
-        v8i P[2];
-        int psc[2];
-        float lsum = 0.f;
-#pragma unroll
-        for (int c = 0; c < 2; c++) {
-            const float mb = __builtin_amdgcn_exp2f(__builtin_fmaf(bmax[c], cl, -m_new));
-            const uint32_t mbits = __builtin_bit_cast(uint32_t, mb);
-            const uint32_t sbyte =
-                (mbits < 0x00800000u) ? 127u : (uint32_t)(scale_exponent_f32<kRule>(mbits) + 127);
-            const float sf = e8m0_as_f32(sbyte);
-            psc[c] = (int)sbyte;
-            uint32_t w[4] = {0, 0, 0, 0};
-#pragma unroll
-            for (int n = 0; n < 32; n += 2) {
-                const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(S[c][n >> 4][n & 15], cl, -m_new));
-                const float p1 =
-                    __builtin_amdgcn_exp2f(__builtin_fmaf(S[c][(n + 1) >> 4][(n + 1) & 15], cl, -m_new));
-                if (!kPnq) lsum += p0 + p1;
-                w[n >> 3] = cvt_fp4x2(w[n >> 3], p0, p1, sf, (n & 7) >> 1);
-            }
-            P[c] = fp4_operand(make_uint4(w[0], w[1], w[2], w[3]));
-        }
-
-        float dl;
-        if (kPnq) {
-            v16f lt;
-#pragma unroll
-            for (int i = 0; i < 16; i++) lt[i] = 0.f;
-            lt = mfma_fp4<0>(ones, P[0], lt, 127, psc[0]);
-            lt = mfma_fp4<0>(ones, P[1], lt, 127, psc[1]);
-            dl = lt[0];
-        } else {
-            dl = lsum;  // this lane's half of the row; halves are added at the end
-        }
-        lacc = alpha * lacc + dl;
-
-        // ---- O~^T = diag(alpha) O~^T + V^T P^T
-        asm volatile("s_waitcnt lgkmcnt(0)"
-                     : "+v"(vr[0][0]), "+v"(vr[0][1]), "+v"(vr[1][0]), "+v"(vr[1][1]), "+v"(vr[2][0]),
-                       "+v"(vr[2][1]), "+v"(vr[3][0]), "+v"(vr[3][1]));
-        v8i vop[4][2];
-#pragma unroll
-        for (int n = 0; n < 4; n++) {
-            vop[n][0] = fp4_v(vr[n][0]);
-            vop[n][1] = fp4_v(vr[n][1]);
-        }
-        if (__any(alpha != 1.f)) {
-#pragma unroll
-            for (int n = 0; n < 4; n++)
-#pragma unroll
-                for (int i = 0; i < 16; i++) O[n][i] *= alpha;
-        }
-#pragma unroll
-        for (int n = 0; n < 4; n++) {
-            const int sreg = n < 2 ? (int)vsb.x : (int)vsb.y;
-            // scale byte index 2n + c within the lane's 8 bytes
-            if ((n & 1) == 0) {
-                O[n] = mfma_fp4<0>(vop[n][0], P[0], O[n], sreg, psc[0]);
-                O[n] = mfma_fp4<1>(vop[n][1], P[1], O[n], sreg, psc[1]);
-            } else {
-                O[n] = mfma_fp4<2>(vop[n][0], P[0], O[n], sreg, psc[0]);
-                O[n] = mfma_fp4<3>(vop[n][1], P[1], O[n], sreg, psc[1]);
-            }
-        }
+        attend_tile<kRule, kPnq>(st, tile, N, q, h, lane, qB0, qB1, qS0, qS1, ones, m, lacc, O);
 
         __builtin_amdgcn_s_waitcnt(0);  // the next tile's direct LDS loads landed
         __syncthreads();
     }
 
-    // ---- O = O~ / l  -> bf16
-    float ltot = lacc;
-    if (!kPnq) ltot += __shfl_xor(lacc, 32);
-    if (qi < Nq) {
-        uint16_t* orow = a.out + (int64_t)(rowbase + qi) * 128;
+    store_rows<kPnq>(a, rowbase, qi, h, lacc, O);
+}
+
+// Short key sequences (cross-attention over a text context, at most
+// kResidentKeys keys): the workgroup copies all of the head's K^ and V^ tiles
+// into LDS once and then runs several query tiles of that head against them,
+// with no per-tile loads or barriers; each query tile is the same computation
+// as in attention_kernel.
+constexpr int kResidentTiles = kResidentKeys / 128;
+
+template <int kRule, bool kPnq>
+__global__ __launch_bounds__(kThreads, 2) void attention_resident_kernel(AttnArgs a) {
+    __shared__ __attribute__((aligned(16))) uint8_t lds[kResidentTiles * kStageBytes];
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lane = tid & 63;
+    const int q = lane & 31, h = lane >> 5;
+
+    const int L = blockIdx.x;
+    const int logical = (L & 7) * a.per_xcd + (L >> 3);
+    if (logical >= a.total_tiles) return;
+    const int bh = logical / a.nchunks;
+    const int chunk = logical - bh * a.nchunks;
+    const int qt0 = chunk * a.qt_per_wg;
+    const int qt1 = min(a.qtiles, qt0 + a.qt_per_wg);
+    const int N = a.N;
+    const int Nq = a.Nq;
+    const int64_t rowbase = (int64_t)bh * Nq;
+    const int ntiles = (N + 127) / 128;
+
+    for (int t = 0; t < ntiles; t++) {
+        load_tile_codes(lds + t * kStageBytes, a, bh, t, wave, lane);
+        load_tile_scales(lds + t * kStageBytes, a, bh, t, wave, lane);
+    }
+
+    v8i ones;
 #pragma unroll
-        for (int n = 0; n < 4; n++) {
-#pragma unroll
-            for (int g = 0; g < 4; g++) {
-                const uint32_t b0 = f32_to_bf16_bits(O[n][4 * g + 0] / ltot);
-                const uint32_t b1 = f32_to_bf16_bits(O[n][4 * g + 1] / ltot);
-                const uint32_t b2 = f32_to_bf16_bits(O[n][4 * g + 2] / ltot);
-                const uint32_t b3 = f32_to_bf16_bits(O[n][4 * g + 3] / ltot);
-                *reinterpret_cast<uint2*>(orow + 32 * n + 8 * g + 4 * h) =
-                    make_uint2(b0 | (b1 << 16), b2 | (b3 << 16));
-            }
+    for (int i = 0; i < 8; i++) ones[i] = i < 4 ? 0x22222222 : 0;
+
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's direct LDS loads landed
+    __syncthreads();                // and every other wave's
+
+    // Q^ operands of the first query tile; each later one is loaded while
+    // the previous tile is processed
+    auto q_row = [&](int qt) { return min(qt * kQueryTile + wave * kQw + q, Nq - 1); };
+    int qic = q_row(qt0);
+    uint4 qa0 = *reinterpret_cast<const uint4*>(a.qc + (rowbase + qic) * 64 + 16 * h);
+    uint4 qa1 = *reinterpret_cast<const uint4*>(a.qc + (rowbase + qic) * 64 + 16 * (2 + h));
+    int qs0 = a.qs[(rowbase + qic) * 4 + h];
+    int qs1 = a.qs[(rowbase + qic) * 4 + 2 + h];
+
+    for (int qt = qt0; qt < qt1; qt++) {
+        const int qi = qt * kQueryTile + wave * kQw + q;
+        const v8i qB0 = fp4_operand(qa0);
+        const v8i qB1 = fp4_operand(qa1);
+        const int qS0 = qs0;
+        const int qS1 = qs1;
+        if (qt + 1 < qt1) {
+            qic = q_row(qt + 1);
+            qa0 = *reinterpret_cast<const uint4*>(a.qc + (rowbase + qic) * 64 + 16 * h);
+            qa1 = *reinterpret_cast<const uint4*>(a.qc + (rowbase + qic) * 64 + 16 * (2 + h));
+            qs0 = a.qs[(rowbase + qic) * 4 + h];
+            qs1 = a.qs[(rowbase + qic) * 4 + 2 + h];
         }
+
+        float m = -__builtin_inff();
+        float lacc = 0.f;
+        v16f O[4];
+#pragma unroll
+        for (int n = 0; n < 4; n++)
+#pragma unroll
+            for (int i = 0; i < 16; i++) O[n][i] = 0.f;
+
+        for (int tile = 0; tile < ntiles; tile++)
+            attend_tile<kRule, kPnq>(lds + tile * kStageBytes, tile, N, q, h, lane, qB0, qB1, qS0, qS1, ones,
+                                     m, lacc, O);
+
+        store_rows<kPnq>(a, rowbase, qi, h, lacc, O);
     }
 }
 
@@ -465,6 +565,14 @@ hipError_t launch_tile_scales(const uint8_t* ks, const uint8_t* vs, uint8_t* out
 
 hipError_t launch_attention(const AttnArgs& a, int mode, hipStream_t stream) {
     const dim3 grid((unsigned)(8 * a.per_xcd));
+    if (a.N <= kResidentKeys) {
+        switch (mode) {
+            case 0: attention_resident_kernel<kRuleOcp, false><<<grid, kThreads, 0, stream>>>(a); break;
+            case 1: attention_resident_kernel<kRuleUos, false><<<grid, kThreads, 0, stream>>>(a); break;
+            default: attention_resident_kernel<kRuleUos, true><<<grid, kThreads, 0, stream>>>(a); break;
+        }
+        return hipGetLastError();
+    }
     switch (mode) {
         case 0: attention_kernel<kRuleOcp, false><<<grid, kThreads, 0, stream>>>(a); break;
         case 1: attention_kernel<kRuleUos, false><<<grid, kThreads, 0, stream>>>(a); break;

@@ -80,13 +80,6 @@ __device__ __forceinline__ float e8m0_as_f32(uint32_t byte) {
     return __builtin_bit_cast(float, byte << 23);
 }
 
-// Round-to-nearest-even fp32 -> bf16 bits (finite inputs).
-__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
-    uint32_t u = __builtin_bit_cast(uint32_t, f);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return u >> 16;
-}
-
 __device__ __forceinline__ v8i fp4_operand(uint4 v) {
     v8i r;
     r[0] = (int)v.x;

@@ -47,9 +47,15 @@ struct AttnArgs {
     int Nq;             // queries per head (Q^ codes/scales and out are [BH, Nq, ...])
     int nb;
     int qtiles;
-    int total_tiles;
+    int total_tiles;    // workgroups that do work
     int per_xcd;
+    int qt_per_wg;      // resident kernel: query tiles per workgroup
+    int nchunks;        // resident kernel: workgroups per (batch, head)
 };
+
+// Keys up to which the whole of K^ and V^ of a head stays in LDS for the
+// workgroup's lifetime (launch_attention then runs the resident kernel).
+constexpr int kResidentKeys = 512;
 
 // Scales of K^ and V^ in the attention kernel's operand order (AttnArgs::sc);
 // out holds tile_scales_bytes(BH, N) bytes.
