@@ -135,14 +135,20 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
     return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
+// kOff is the instruction's 16-bit immediate byte offset, so one address
+// register per lane serves every read of a stage.
+template <int kOff = 0>
 __device__ __forceinline__ v4i lds_read128(uint32_t addr) {
+    static_assert(kOff >= 0 && kOff < 65536, "ds offset is 16 bits");
     v4i r;
-    asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(addr));
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(kOff));
     return r;
 }
+template <int kOff = 0>
 __device__ __forceinline__ uint2 lds_read64(uint32_t addr) {
+    static_assert(kOff >= 0 && kOff < 65536, "ds offset is 16 bits");
     uint2 r;
-    asm volatile("ds_read_b64 %0, %1" : "=v"(r) : "v"(addr));
+    asm volatile("ds_read_b64 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(kOff));
     return r;
 }
 __device__ __forceinline__ v8i fp4_v(v4i x) {
@@ -180,21 +186,27 @@ __device__ __forceinline__ void attend_tile(const uint8_t* st, int tile, int N, 
                                             const v8i& qB0, const v8i& qB1, int qS0, int qS1,
                                             const v8i& ones, float& m, float& lacc, v16f (&O)[4]) {
     const float cl = 0.12751743082459868f;  // fp32(log2(e) / sqrt(128))
-    uint2 ksb = lds_read64(lds_addr(st + kKsOff + lane * 8));
-    uint2 vsb = lds_read64(lds_addr(st + kVsOff + lane * 8));
+    // Per-lane LDS addresses of this stage: the scale slot, and the two
+    // 16-byte slots of row q (rows 32 i + q share q's swizzle); every other
+    // row and region is an immediate offset.
+    const uint32_t sbase = lds_addr(st);
+    const uint32_t a_sc = sbase + lane * 8;
+    const uint32_t a_lo = sbase + q * 64 + 16 * ((0 + h) ^ swz(q));
+    const uint32_t a_hi = sbase + q * 64 + 16 * ((2 + h) ^ swz(q));
+    uint2 ksb = lds_read64<kKsOff>(a_sc);
+    uint2 vsb = lds_read64<kVsOff>(a_sc);
 
-    // ---- K^ operands for the 8 S products (chunk c, tile j, half hf)
+    // ---- K^ operands for the 8 S products (chunk c, tile j, half hf):
+    // row 64 c + 32 j + q
     v4i kr[2][2][2];
-#pragma unroll
-    for (int c = 0; c < 2; c++)
-#pragma unroll
-        for (int j = 0; j < 2; j++) {
-            const int row = 64 * c + 32 * j + q;
-            const uint8_t* rp = st + kKcOff + row * 64;
-            const int sw = swz(row);
-            kr[c][j][0] = lds_read128(lds_addr(rp + 16 * ((0 + h) ^ sw)));
-            kr[c][j][1] = lds_read128(lds_addr(rp + 16 * ((2 + h) ^ sw)));
-        }
+    kr[0][0][0] = lds_read128<kKcOff + 0 * 2048>(a_lo);
+    kr[0][0][1] = lds_read128<kKcOff + 0 * 2048>(a_hi);
+    kr[0][1][0] = lds_read128<kKcOff + 1 * 2048>(a_lo);
+    kr[0][1][1] = lds_read128<kKcOff + 1 * 2048>(a_hi);
+    kr[1][0][0] = lds_read128<kKcOff + 2 * 2048>(a_lo);
+    kr[1][0][1] = lds_read128<kKcOff + 2 * 2048>(a_hi);
+    kr[1][1][0] = lds_read128<kKcOff + 3 * 2048>(a_lo);
+    kr[1][1][1] = lds_read128<kKcOff + 3 * 2048>(a_hi);
     asm volatile("s_waitcnt lgkmcnt(0)"
                  : "+v"(kr[0][0][0]), "+v"(kr[0][0][1]), "+v"(kr[0][1][0]), "+v"(kr[0][1][1]),
                    "+v"(kr[1][0][0]), "+v"(kr[1][0][1]), "+v"(kr[1][1][0]), "+v"(kr[1][1][1]), "+v"(ksb),
@@ -229,16 +241,17 @@ __device__ __forceinline__ void attend_tile(const uint8_t* st, int tile, int N, 
         }
     }
 
-    // ---- V^ operands for the PV products (read now, used after softmax)
+    // ---- V^ operands for the PV products (read now, used after softmax):
+    // row (channel) 32 n + q
     v4i vr[4][2];
-#pragma unroll
-    for (int n = 0; n < 4; n++) {
-        const int row = 32 * n + q;
-        const uint8_t* rp = st + kVcOff + row * 64;
-        const int sw = swz(row);
-        vr[n][0] = lds_read128(lds_addr(rp + 16 * ((0 + h) ^ sw)));
-        vr[n][1] = lds_read128(lds_addr(rp + 16 * ((2 + h) ^ sw)));
-    }
+    vr[0][0] = lds_read128<kVcOff + 0 * 2048>(a_lo);
+    vr[0][1] = lds_read128<kVcOff + 0 * 2048>(a_hi);
+    vr[1][0] = lds_read128<kVcOff + 1 * 2048>(a_lo);
+    vr[1][1] = lds_read128<kVcOff + 1 * 2048>(a_hi);
+    vr[2][0] = lds_read128<kVcOff + 2 * 2048>(a_lo);
+    vr[2][1] = lds_read128<kVcOff + 2 * 2048>(a_hi);
+    vr[3][0] = lds_read128<kVcOff + 3 * 2048>(a_lo);
+    vr[3][1] = lds_read128<kVcOff + 3 * 2048>(a_hi);
 
     // ---- mask keys past the end of the sequence (last tile only)
     const int k0 = tile * 128;
