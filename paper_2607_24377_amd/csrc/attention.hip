@@ -296,14 +296,18 @@ __device__ __forceinline__ void attend_tile(const uint8_t* st, int tile, int N, 
             (mbits < 0x00800000u) ? 127u : (uint32_t)(scale_exponent_f32<kRule>(mbits) + 127);
         const float sf = e8m0_as_f32(sbyte);
         psc[c] = (int)sbyte;
-        uint32_t w[4] = {0, 0, 0, 0};
+        uint32_t w[4];
 #pragma unroll
         for (int n = 0; n < 32; n += 2) {
             const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(S[c][n >> 4][n & 15], cl, -m_new));
             const float p1 =
                 __builtin_amdgcn_exp2f(__builtin_fmaf(S[c][(n + 1) >> 4][(n + 1) & 15], cl, -m_new));
             if (!kPnq) lsum += p0 + p1;
-            w[n >> 3] = cvt_fp4x2(w[n >> 3], p0, p1, sf, (n & 7) >> 1);
+            // a word's four conversions write all of its bytes, so the first
+            // one starts from p0's own register (dead afterwards) rather
+            // than from a zeroed one
+            const uint32_t prev = (n & 7) == 0 ? __builtin_bit_cast(uint32_t, p0) : w[n >> 3];
+            w[n >> 3] = cvt_fp4x2(prev, p0, p1, sf, (n & 7) >> 1);
         }
         P[c] = fp4_operand(make_uint4(w[0], w[1], w[2], w[3]));
     }
