@@ -4,7 +4,10 @@ video queries attending to a short text context, Sec. 5.1).
 Output against the oracle fed the GPU's own codes (same tolerance as
 self-attention), for ragged query and key lengths, every mode; the forward
 equals attend() on separately quantized operands; with Nq = Nkv the cross
-entry points equal the self-attention ones.
+entry points equal the self-attention ones.  Up to 512 keys the K^/V^ of a
+head stay resident in LDS and a workgroup runs several query tiles: lengths
+on both sides of 512 and a case with two query tiles per workgroup and a
+lone last one are covered.
 """
 import numpy as np
 import pytest
@@ -60,7 +63,8 @@ def test_cross_ragged_all_rows(mx, mode):
 
 
 @pytest.mark.parametrize("Nq,Nkv", [(200, 1), (200, 31), (1, 200), (129, 32), (130, 33), (300, 128),
-                                    (64, 129), (257, 255)])
+                                    (64, 129), (257, 255), (300, 512), (300, 513), (130, 640),
+                                    (64, 1100)])
 def test_cross_ragged_lengths(mx, Nq, Nkv):
     w = inputs.Workload(60 + Nkv % 5, f"cross_{Nq}x{Nkv}", 2, 2, Nq, 128, "cross", Nkv=Nkv)
     for mode in ("ocp_vanilla", "uos_pnq"):
@@ -78,3 +82,12 @@ def test_equal_lengths_match_self_attention(mx):
     w = inputs.custom(1, 2, 300, kind="video", index=9)
     q, k, v = (mx.bf16_from_bits(x) for x in inputs.generate(w))
     assert torch.equal(mx.cross_forward(q, k, v, "uos_pnq"), mx.forward(q, k, v, "uos_pnq"))
+
+
+def test_resident_several_query_tiles_per_workgroup(mx):
+    # 16 heads x 129 query tiles = 2064 tiles: two per workgroup, the last
+    # workgroup of each head gets one
+    w = inputs.Workload(71, "cross_16x16500x500", 1, 16, 16500, 128, "cross", Nkv=500)
+    for mode in ("ocp_vanilla", "uos_pnq"):
+        _check(mx, w, mode, [0, 7, 15], 40, w.name)
+    torch.cuda.empty_cache()
