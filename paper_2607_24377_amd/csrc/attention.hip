@@ -5,8 +5,8 @@
 // B_c) in increasing order, as Algorithm 2 does, and for each tile:
 //
 //   1. reads the tile's MXFP4 K^ and V^ codes and E8M0 scales from LDS (the
-//      next tile is already in flight into the other LDS buffer: codes by
-//      direct global->LDS loads, scales through four registers per thread);
+//      next tile is already in flight into the other LDS buffer, copied by
+//      buffer loads straight into LDS);
 //   2. S^T = K^ Q^T on the block-scaled FP4 matrix cores
 //      (V_MFMA_SCALE_F32_32X32X64_F8F6F4, fp32 accumulation);
 //   3. online softmax in registers: running maximum m, correction
@@ -18,7 +18,9 @@
 //   5. l = alpha*l + sum(P~) (direct placement, Eq. direct_mxfp4_tile) or
 //      l = alpha*l + sum(P^) (PNQ, Eq. pnq_online_update);  the PNQ row sum
 //      of the dequantized P^ is taken on the matrix cores as ones * P^T;
-//   6. O~^T = diag(alpha) O~^T + V^T P^T on the FP4 matrix cores.
+//   6. O~^T = diag(alpha) O~^T + V^T P^T on the FP4 matrix cores, one
+//      64-key chunk at a time, so the first chunk's products run while the
+//      second chunk's P~ is formed.
 //
 // After the last tile O = O~ / l is rounded to bf16 (Eq.
 // online_attention_output).
@@ -83,48 +85,109 @@ typedef __attribute__((address_space(1))) void* gbl_ptr_t;
 // to LDS base + 16*i, so each lane fetches whatever chunk belongs at its slot
 // of the permuted, swizzled layout.  Nothing passes through VGPRs; completion
 // is tracked by vmcnt.  Wave w copies LDS bytes [2048 w, 2048 w + 2048) of
-// each of the two 8 KiB code regions.
-__device__ __forceinline__ void load_tile_codes(uint8_t* st, const AttnArgs& a, int bh, int tile,
-                                                int wave, int lane) {
-    const int N = a.N, nb = a.nb;
-    const int k0 = tile * 128;
-    const int64_t krow0 = (int64_t)bh * N;
-    const int64_t vrow0 = (int64_t)bh * 128;
-#pragma unroll
-    for (int it = 0; it < 2; it++) {
-        const int p = (2 * wave + it) * 64 + lane;  // 16-byte slot of the region
-        const int row = p >> 2, slot = p & 3;
-        // K^: row -> (chunk c, tile j, A-row r) -> key; slot -> channel block
-        const int r = row & 31, j = (row >> 5) & 1, c = row >> 6;
-        const int key = 64 * c + 32 * ((r >> 2) & 1) + 16 * j + 4 * (r >> 3) + (r & 3);
-        const int gk = min(k0 + key, N - 1);  // keys past N: masked scores
-        const int db = slot ^ swz(row);
-        const uint8_t* ksrc = (a.kc + krow0 * 64) + (uint32_t)(gk * 64 + db * 16);
-        __builtin_amdgcn_global_load_lds((gbl_ptr_t)ksrc, (lds_ptr_t)(st + kKcOff + (2 * wave + it) * 1024), 16, 0, 0);
-        // V^: row = channel, slot -> key block of the tile (blocks past the
-        // end read the last block; the matching P^ entries are zero)
-        const int kb = slot ^ swz(row);
-        const int blk = min(4 * tile + kb, nb - 1);
-        const uint8_t* vsrc = (a.vc + vrow0 * nb * 16) + (uint32_t)((row * nb + blk) * 16);
-        __builtin_amdgcn_global_load_lds((gbl_ptr_t)vsrc, (lds_ptr_t)(st + kVcOff + (2 * wave + it) * 1024), 16, 0, 0);
-    }
-}
+// each of the two 8 KiB code regions, and wave 0 also the tile's K^ and V^
+// scales, already in the lanes' MFMA operand order (tile_scales_kernel).
+// Each source is a buffer resource over one head's array: a lane's offset
+// within a tile is fixed, the tile's offset is a scalar, so no per-tile
+// address arithmetic runs on the vector units.  Bytes past the end of an
+// array read as zero (buffer range check): the K^ rows of keys past N (their
+// scores are masked) and the V^ key blocks past the end (the matching P^
+// entries are zero) contribute nothing.
+struct TileLoader {
+    __amdgpu_buffer_rsrc_t kc;  // this head's K^ codes [N, 64]
+    __amdgpu_buffer_rsrc_t vc;  // this head's V^ codes [128, nb * 16]
+    __amdgpu_buffer_rsrc_t sc;  // this head's operand-order scales [ntiles, 1024]
+    uint32_t koff[2];           // lane offsets (bytes) within a tile
+    uint32_t voff[2];
+    int wave, lane;
 
-// The tile's K^ and V^ scales, already in the lanes' MFMA operand order (see
-// tile_scales_kernel): one 1 KiB direct load by wave 0 into [kKsOff, kStageBytes).
-__device__ __forceinline__ void load_tile_scales(uint8_t* st, const AttnArgs& a, int bh, int tile, int wave,
-                                                 int lane) {
-    if (wave != 0) return;
-    const int ntiles = (a.N + 127) / 128;
-    const uint8_t* src = a.sc + ((int64_t)bh * ntiles + tile) * 1024 + lane * 16;
-    __builtin_amdgcn_global_load_lds((gbl_ptr_t)src, (lds_ptr_t)(st + kKsOff), 16, 0, 0);
+    // raw buffer, 32-bit data format (word 3 of the gfx9 buffer descriptor)
+    static constexpr int kRsrcFlags = 0x00020000;
+
+    __device__ __forceinline__ TileLoader(const AttnArgs& a, int bh, int wave_, int lane_)
+        : wave(wave_), lane(lane_) {
+        const int ntiles = (a.N + 127) / 128;
+        kc = __builtin_amdgcn_make_buffer_rsrc((void*)(a.kc + (int64_t)bh * a.N * 64), 0, a.N * 64, kRsrcFlags);
+        vc = __builtin_amdgcn_make_buffer_rsrc((void*)(a.vc + (int64_t)bh * 128 * a.nb * 16), 0,
+                                               128 * a.nb * 16, kRsrcFlags);
+        sc = __builtin_amdgcn_make_buffer_rsrc((void*)(a.sc + (int64_t)bh * ntiles * 1024), 0, ntiles * 1024,
+                                               kRsrcFlags);
+#pragma unroll
+        for (int it = 0; it < 2; it++) {
+            const int p = (2 * wave + it) * 64 + lane;  // 16-byte slot of the region
+            const int row = p >> 2;
+            // K^: row -> (chunk c, tile j, A-row r) -> key; slot -> channel
+            // block.  V^: row = channel, slot -> key block (same swizzle).
+            const int r = row & 31, j = (row >> 5) & 1, c = row >> 6;
+            const int key = 64 * c + 32 * ((r >> 2) & 1) + 16 * j + 4 * (r >> 3) + (r & 3);
+            const int db = (p & 3) ^ swz(row);
+            koff[it] = (uint32_t)(key * 64 + db * 16);
+            voff[it] = (uint32_t)((row * a.nb + db) * 16);
+        }
+    }
+
+    __device__ __forceinline__ void load(uint8_t* st, int tile) const {
+#pragma unroll
+        for (int it = 0; it < 2; it++) {
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(kc, (lds_ptr_t)(st + kKcOff + (2 * wave + it) * 1024), 16,
+                                                     (int)koff[it], tile * 8192, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(vc, (lds_ptr_t)(st + kVcOff + (2 * wave + it) * 1024), 16,
+                                                     (int)voff[it], tile * 64, 0, 0);
+        }
+        if (wave == 0)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(sc, (lds_ptr_t)(st + kKsOff), 16, lane * 16, tile * 1024, 0, 0);
+    }
+};
+
+// Maxima of scores, which are finite or -inf (masked keys), never NaN: the
+// NaN-propagating maximum needs no quieting of its operands and fuses into
+// the 3-input form.
+__device__ __forceinline__ float max2f(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+__device__ __forceinline__ float max3f(float a, float b, float c) { return max2f(max2f(a, b), c); }
+
+// Largest of the 32 scores of one P~ block (the lane's 16 + 16 accumulators
+// of the two 32-key S products of a chunk): two independent chains.
+__device__ __forceinline__ float block_max32(const v16f& a, const v16f& b) {
+    float x = max3f(a[0], a[1], a[2]);
+    float y = max3f(b[0], b[1], b[2]);
+#pragma unroll
+    for (int i = 3; i < 15; i += 2) {
+        x = max3f(x, a[i], a[i + 1]);
+        y = max3f(y, b[i], b[i + 1]);
+    }
+    return max2f(max3f(x, a[15], b[15]), y);
 }
 
 __device__ __forceinline__ float max_with_other_half(float x) {
     // lanes l and l^32 hold the two halves of one query row
     const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, x),
                                                     __builtin_bit_cast(uint32_t, x), false, false);
-    return fmaxf(__builtin_bit_cast(float, (uint32_t)r[0]), __builtin_bit_cast(float, (uint32_t)r[1]));
+    return max2f(__builtin_bit_cast(float, (uint32_t)r[0]), __builtin_bit_cast(float, (uint32_t)r[1]));
+}
+
+// c * x rounded towards -inf: the round-to-nearest product, stepped one ulp
+// down when it exceeds the exact product (the FMA gives the exact residual).
+// x is finite.
+__device__ __forceinline__ float mul_rd(float c, float x) {
+    const float u = c * x;
+    const uint32_t ub = __builtin_bit_cast(uint32_t, u);
+    // one ulp towards -inf: magnitude down for u > 0, up for u < 0 (and
+    // -0 -> the negative denormal); u = +0 never rounds up a negative product
+    const uint32_t down = ub - (uint32_t)(((int32_t)ub >> 31) | 1);
+    return __builtin_bit_cast(float, __builtin_fmaf(c, x, -u) < 0.f ? down : ub);
+}
+
+// E8M0 byte of a P~ block from the bits of its maximum M (0 <= M <= 1 + 2^-20):
+// e + 127 = E - 2 under the OCP floor rule and E - 2 + [fraction > 0x680000]
+// under UOS (as scale_exponent_f32), where adding 0x17FFFF carries into the
+// exponent field exactly when the 23-bit fraction exceeds 0x680000; clamped
+// at byte 0 (e >= -127).  A block whose maximum underflowed to 0 holds only
+// zeros, so its codes are all zero and its scale affects nothing: it gets
+// byte 0 here rather than the 127 of an all-zero input block.
+template <int kRule>
+__device__ __forceinline__ uint32_t p_scale_byte(uint32_t mbits) {
+    const int E = (int)((mbits + (kRule == kRuleUos ? 0x17FFFFu : 0u)) >> 23);
+    return (uint32_t)max(E - 2, 0);
 }
 
 // LDS reads issued as inline assembly.  The compiler does not see them as LDS
@@ -178,35 +241,41 @@ __device__ __forceinline__ uint32_t cvt_fp4x2(uint32_t old, float a, float b, fl
     }
 }
 
-// One KV tile of Algorithm 2 for the wave's 32 query rows, on the tile's
-// stage in LDS: S^T = K^ Q^T, the online-softmax update of (m, l), P^ and
-// O~^T += V^T P^T.  Reads LDS only; the caller owns loads and barriers.
-template <int kRule, bool kPnq>
-__device__ __forceinline__ void attend_tile(const uint8_t* st, int tile, int N, int q, int h, int lane,
+// Per-lane LDS addresses of the stage at `st`: the lane's 8-byte scale slot
+// and the two 16-byte slots of row q (rows 32 i + q share q's swizzle); every
+// other row and region, and the second stage, are immediate offsets.
+struct LdsLane {
+    uint32_t sc, lo, hi;
+};
+__device__ __forceinline__ LdsLane lds_lane(const uint8_t* st, int q, int h, int lane) {
+    const uint32_t base = lds_addr(st);
+    return {base + lane * 8, base + q * 64 + 16 * ((0 + h) ^ swz(q)), base + q * 64 + 16 * ((2 + h) ^ swz(q))};
+}
+
+// One KV tile of Algorithm 2 for the wave's 32 query rows, on LDS stage
+// kStage (relative to la): S^T = K^ Q^T, the online-softmax update of (m, l),
+// P^ and O~^T += V^T P^T.  Reads LDS only; the caller owns loads and barriers.
+template <int kRule, bool kPnq, int kStage>
+__device__ __forceinline__ void attend_tile(const LdsLane& la, int tile, int N, int h,
                                             const v8i& qB0, const v8i& qB1, int qS0, int qS1,
                                             const v8i& ones, float& m, float& lacc, v16f (&O)[4]) {
     const float cl = 0.12751743082459868f;  // fp32(log2(e) / sqrt(128))
-    // Per-lane LDS addresses of this stage: the scale slot, and the two
-    // 16-byte slots of row q (rows 32 i + q share q's swizzle); every other
-    // row and region is an immediate offset.
-    const uint32_t sbase = lds_addr(st);
-    const uint32_t a_sc = sbase + lane * 8;
-    const uint32_t a_lo = sbase + q * 64 + 16 * ((0 + h) ^ swz(q));
-    const uint32_t a_hi = sbase + q * 64 + 16 * ((2 + h) ^ swz(q));
-    uint2 ksb = lds_read64<kKsOff>(a_sc);
-    uint2 vsb = lds_read64<kVsOff>(a_sc);
+    constexpr int so = kStage * kStageBytes;
+    const uint32_t a_sc = la.sc, a_lo = la.lo, a_hi = la.hi;
+    uint2 ksb = lds_read64<so + kKsOff>(a_sc);
+    uint2 vsb = lds_read64<so + kVsOff>(a_sc);
 
     // ---- K^ operands for the 8 S products (chunk c, tile j, half hf):
     // row 64 c + 32 j + q
     v4i kr[2][2][2];
-    kr[0][0][0] = lds_read128<kKcOff + 0 * 2048>(a_lo);
-    kr[0][0][1] = lds_read128<kKcOff + 0 * 2048>(a_hi);
-    kr[0][1][0] = lds_read128<kKcOff + 1 * 2048>(a_lo);
-    kr[0][1][1] = lds_read128<kKcOff + 1 * 2048>(a_hi);
-    kr[1][0][0] = lds_read128<kKcOff + 2 * 2048>(a_lo);
-    kr[1][0][1] = lds_read128<kKcOff + 2 * 2048>(a_hi);
-    kr[1][1][0] = lds_read128<kKcOff + 3 * 2048>(a_lo);
-    kr[1][1][1] = lds_read128<kKcOff + 3 * 2048>(a_hi);
+    kr[0][0][0] = lds_read128<so + kKcOff + 0 * 2048>(a_lo);
+    kr[0][0][1] = lds_read128<so + kKcOff + 0 * 2048>(a_hi);
+    kr[0][1][0] = lds_read128<so + kKcOff + 1 * 2048>(a_lo);
+    kr[0][1][1] = lds_read128<so + kKcOff + 1 * 2048>(a_hi);
+    kr[1][0][0] = lds_read128<so + kKcOff + 2 * 2048>(a_lo);
+    kr[1][0][1] = lds_read128<so + kKcOff + 2 * 2048>(a_hi);
+    kr[1][1][0] = lds_read128<so + kKcOff + 3 * 2048>(a_lo);
+    kr[1][1][1] = lds_read128<so + kKcOff + 3 * 2048>(a_hi);
     asm volatile("s_waitcnt lgkmcnt(0)"
                  : "+v"(kr[0][0][0]), "+v"(kr[0][0][1]), "+v"(kr[0][1][0]), "+v"(kr[0][1][1]),
                    "+v"(kr[1][0][0]), "+v"(kr[1][0][1]), "+v"(kr[1][1][0]), "+v"(kr[1][1][1]), "+v"(ksb),
@@ -244,14 +313,14 @@ __device__ __forceinline__ void attend_tile(const uint8_t* st, int tile, int N, 
     // ---- V^ operands for the PV products (read now, used after softmax):
     // row (channel) 32 n + q
     v4i vr[4][2];
-    vr[0][0] = lds_read128<kVcOff + 0 * 2048>(a_lo);
-    vr[0][1] = lds_read128<kVcOff + 0 * 2048>(a_hi);
-    vr[1][0] = lds_read128<kVcOff + 1 * 2048>(a_lo);
-    vr[1][1] = lds_read128<kVcOff + 1 * 2048>(a_hi);
-    vr[2][0] = lds_read128<kVcOff + 2 * 2048>(a_lo);
-    vr[2][1] = lds_read128<kVcOff + 2 * 2048>(a_hi);
-    vr[3][0] = lds_read128<kVcOff + 3 * 2048>(a_lo);
-    vr[3][1] = lds_read128<kVcOff + 3 * 2048>(a_hi);
+    vr[0][0] = lds_read128<so + kVcOff + 0 * 2048>(a_lo);
+    vr[0][1] = lds_read128<so + kVcOff + 0 * 2048>(a_hi);
+    vr[1][0] = lds_read128<so + kVcOff + 1 * 2048>(a_lo);
+    vr[1][1] = lds_read128<so + kVcOff + 1 * 2048>(a_hi);
+    vr[2][0] = lds_read128<so + kVcOff + 2 * 2048>(a_lo);
+    vr[2][1] = lds_read128<so + kVcOff + 2 * 2048>(a_hi);
+    vr[3][0] = lds_read128<so + kVcOff + 3 * 2048>(a_lo);
+    vr[3][1] = lds_read128<so + kVcOff + 3 * 2048>(a_hi);
 
     // ---- mask keys past the end of the sequence (last tile only)
     const int k0 = tile * 128;
@@ -265,67 +334,19 @@ __device__ __forceinline__ void attend_tile(const uint8_t* st, int tile, int N, 
                     if (k0 + 64 * c + 32 * h + 16 * j + i >= N) S[c][j][i] = -__builtin_inff();
     }
 
-    // ---- running maximum
+    // ---- running maximum: the block maxima (one P~ block per lane and
+    // chunk), the tile maximum of the row across the lane pair
     float bmax[2];
 #pragma unroll
-    for (int c = 0; c < 2; c++) {
-        float mx = S[c][0][0];
-#pragma unroll
-        for (int j = 0; j < 2; j++)
-#pragma unroll
-            for (int i = 0; i < 16; i++) mx = fmaxf(mx, S[c][j][i]);
-        bmax[c] = mx;
-    }
-    float rmax = fmaxf(bmax[0], bmax[1]);
-    rmax = max_with_other_half(rmax);
-    float u = cl * rmax;
-    if (__builtin_fmaf(rmax, cl, -u) < 0.f) u = next_down(u);  // RD(c * max s)
-    const float m_new = fmaxf(m, u);
+    for (int c = 0; c < 2; c++) bmax[c] = block_max32(S[c][0], S[c][1]);
+    float rmax = max_with_other_half(max2f(bmax[0], bmax[1]));
+    const float m_new = max2f(m, mul_rd(cl, rmax));
     const float alpha = __builtin_amdgcn_exp2f(m - m_new);  // 0 on the first tile
     m = m_new;
 
-    // ---- P~, its MXFP4 quantization P^, row-sum contribution
-    v8i P[2];
-    int psc[2];
-    float lsum = 0.f;
-#pragma unroll
-    for (int c = 0; c < 2; c++) {
-        const float mb = __builtin_amdgcn_exp2f(__builtin_fmaf(bmax[c], cl, -m_new));
-        const uint32_t mbits = __builtin_bit_cast(uint32_t, mb);
-        const uint32_t sbyte =
-            (mbits < 0x00800000u) ? 127u : (uint32_t)(scale_exponent_f32<kRule>(mbits) + 127);
-        const float sf = e8m0_as_f32(sbyte);
-        psc[c] = (int)sbyte;
-        uint32_t w[4];
-#pragma unroll
-        for (int n = 0; n < 32; n += 2) {
-            const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(S[c][n >> 4][n & 15], cl, -m_new));
-            const float p1 =
-                __builtin_amdgcn_exp2f(__builtin_fmaf(S[c][(n + 1) >> 4][(n + 1) & 15], cl, -m_new));
-            if (!kPnq) lsum += p0 + p1;
-            // a word's four conversions write all of its bytes, so the first
-            // one starts from p0's own register (dead afterwards) rather
-            // than from a zeroed one
-            const uint32_t prev = (n & 7) == 0 ? __builtin_bit_cast(uint32_t, p0) : w[n >> 3];
-            w[n >> 3] = cvt_fp4x2(prev, p0, p1, sf, (n & 7) >> 1);
-        }
-        P[c] = fp4_operand(make_uint4(w[0], w[1], w[2], w[3]));
-    }
-
-    float dl;
-    if (kPnq) {
-        v16f lt;
-#pragma unroll
-        for (int i = 0; i < 16; i++) lt[i] = 0.f;
-        lt = mfma_fp4<0>(ones, P[0], lt, 127, psc[0]);
-        lt = mfma_fp4<0>(ones, P[1], lt, 127, psc[1]);
-        dl = lt[0];
-    } else {
-        dl = lsum;  // this lane's half of the row; halves are added at the end
-    }
-    lacc = alpha * lacc + dl;
-
-    // ---- O~^T = diag(alpha) O~^T + V^T P^T
+    // ---- O~^T rescale and V^ operands, then per 64-key chunk: P~ -> P^ and
+    // that chunk's PV products (so chunk 0's products run under chunk 1's
+    // softmax)
     asm volatile("s_waitcnt lgkmcnt(0)"
                  : "+v"(vr[0][0]), "+v"(vr[0][1]), "+v"(vr[1][0]), "+v"(vr[1][1]), "+v"(vr[2][0]),
                    "+v"(vr[2][1]), "+v"(vr[3][0]), "+v"(vr[3][1]));
@@ -341,19 +362,42 @@ __device__ __forceinline__ void attend_tile(const uint8_t* st, int tile, int N, 
 #pragma unroll
             for (int i = 0; i < 16; i++) O[n][i] *= alpha;
     }
+    float lsum = 0.f;
+    v16f lt;
 #pragma unroll
-    for (int n = 0; n < 4; n++) {
-        const int sreg = n < 2 ? (int)vsb.x : (int)vsb.y;
-        // scale byte index 2n + c within the lane's 8 bytes
-        if ((n & 1) == 0) {
-            O[n] = mfma_fp4<0>(vop[n][0], P[0], O[n], sreg, psc[0]);
-            O[n] = mfma_fp4<1>(vop[n][1], P[1], O[n], sreg, psc[1]);
+    for (int i = 0; i < 16; i++) lt[i] = 0.f;
+#pragma unroll
+    for (int c = 0; c < 2; c++) {
+        const float mb = __builtin_amdgcn_exp2f(__builtin_fmaf(bmax[c], cl, -m_new));
+        const uint32_t sbyte = p_scale_byte<kRule>(__builtin_bit_cast(uint32_t, mb));
+        const float sf = e8m0_as_f32(sbyte);
+        const int psc = (int)sbyte;
+        uint32_t w[4];
+#pragma unroll
+        for (int n = 0; n < 32; n += 2) {
+            const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(S[c][n >> 4][n & 15], cl, -m_new));
+            const float p1 =
+                __builtin_amdgcn_exp2f(__builtin_fmaf(S[c][(n + 1) >> 4][(n + 1) & 15], cl, -m_new));
+            if (!kPnq) lsum += p0 + p1;
+            const uint32_t prev = (n & 7) == 0 ? __builtin_bit_cast(uint32_t, p0) : w[n >> 3];
+            w[n >> 3] = cvt_fp4x2(prev, p0, p1, sf, (n & 7) >> 1);
+        }
+        const v8i P = fp4_operand(make_uint4(w[0], w[1], w[2], w[3]));
+        if (kPnq) lt = mfma_fp4<0>(ones, P, lt, 127, psc);
+        // scale byte 2 (n & 1) + c of the register of channel rows 32 n
+        if (c == 0) {
+            O[0] = mfma_fp4<0>(vop[0][0], P, O[0], (int)vsb.x, psc);
+            O[1] = mfma_fp4<2>(vop[1][0], P, O[1], (int)vsb.x, psc);
+            O[2] = mfma_fp4<0>(vop[2][0], P, O[2], (int)vsb.y, psc);
+            O[3] = mfma_fp4<2>(vop[3][0], P, O[3], (int)vsb.y, psc);
         } else {
-            O[n] = mfma_fp4<2>(vop[n][0], P[0], O[n], sreg, psc[0]);
-            O[n] = mfma_fp4<3>(vop[n][1], P[1], O[n], sreg, psc[1]);
+            O[0] = mfma_fp4<1>(vop[0][1], P, O[0], (int)vsb.x, psc);
+            O[1] = mfma_fp4<3>(vop[1][1], P, O[1], (int)vsb.x, psc);
+            O[2] = mfma_fp4<1>(vop[2][1], P, O[2], (int)vsb.y, psc);
+            O[3] = mfma_fp4<3>(vop[3][1], P, O[3], (int)vsb.y, psc);
         }
     }
-
+    lacc = alpha * lacc + (kPnq ? lt[0] : lsum);  // direct: this lane's half of the row
 }
 
 // O = O~ / l rounded to bf16 (Eq. online_attention_output), as O~ times the
@@ -407,8 +451,8 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
     const int qic = min(qi, Nq - 1);
     const int ntiles = (N + 127) / 128;
 
-    load_tile_codes(lds, a, bh, 0, wave, lane);
-    load_tile_scales(lds, a, bh, 0, wave, lane);
+    const TileLoader loader(a, bh, wave, lane);
+    loader.load(lds, 0);
 
     // Q^ as the B operand of S^T = K^ Q^T: lane (q, h) holds channel block
     // 2*hf + h of its query for the product over channels 64*hf..64*hf+63.
@@ -419,9 +463,12 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
     const int qS1 = a.qs[(rowbase + qic) * 4 + 2 + h];
 
     // FP4 1.0 (code 0b0010) in every position: ones * P^T gives the row sums
+    // (opaque to the compiler, so it stays in VGPRs rather than being copied
+    // from scalar registers every tile)
     v8i ones;
 #pragma unroll
     for (int i = 0; i < 8; i++) ones[i] = i < 4 ? 0x22222222 : 0;
+    asm volatile("" : "+v"(ones));
 
     float m = -__builtin_inff();
     float lacc = 0.f;
@@ -434,18 +481,21 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
     __builtin_amdgcn_s_waitcnt(0);  // direct LDS loads of tile 0 landed
     __syncthreads();
 
-    for (int tile = 0; tile < ntiles; tile++) {
-        const uint8_t* st = lds + (tile & 1) * kStageBytes;
-        uint8_t* next = lds + ((tile + 1) & 1) * kStageBytes;
-        if (tile + 1 < ntiles) {
-            load_tile_codes(next, a, bh, tile + 1, wave, lane);
-            load_tile_scales(next, a, bh, tile + 1, wave, lane);
-        }
-
-        attend_tile<kRule, kPnq>(st, tile, N, q, h, lane, qB0, qB1, qS0, qS1, ones, m, lacc, O);
-
+    // two tiles per trip: stage 0 holds the even tiles, stage 1 the odd ones,
+    // so every LDS address is a lane register plus an immediate
+    const LdsLane la = lds_lane(lds, q, h, lane);
+    for (int tile = 0;; tile += 2) {
+        if (tile + 1 < ntiles) loader.load(lds + kStageBytes, tile + 1);
+        attend_tile<kRule, kPnq, 0>(la, tile, N, h, qB0, qB1, qS0, qS1, ones, m, lacc, O);
         __builtin_amdgcn_s_waitcnt(0);  // the next tile's direct LDS loads landed
         __syncthreads();
+        if (tile + 1 >= ntiles) break;
+
+        if (tile + 2 < ntiles) loader.load(lds, tile + 2);
+        attend_tile<kRule, kPnq, 1>(la, tile + 1, N, h, qB0, qB1, qS0, qS1, ones, m, lacc, O);
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (tile + 2 >= ntiles) break;
     }
 
     store_rows<kPnq>(a, rowbase, qi, h, lacc, O);
@@ -478,10 +528,8 @@ __global__ __launch_bounds__(kThreads, 2) void attention_resident_kernel(AttnArg
     const int64_t rowbase = (int64_t)bh * Nq;
     const int ntiles = (N + 127) / 128;
 
-    for (int t = 0; t < ntiles; t++) {
-        load_tile_codes(lds + t * kStageBytes, a, bh, t, wave, lane);
-        load_tile_scales(lds + t * kStageBytes, a, bh, t, wave, lane);
-    }
+    const TileLoader loader(a, bh, wave, lane);
+    for (int t = 0; t < ntiles; t++) loader.load(lds + t * kStageBytes, t);
 
     v8i ones;
 #pragma unroll
@@ -522,8 +570,8 @@ __global__ __launch_bounds__(kThreads, 2) void attention_resident_kernel(AttnArg
             for (int i = 0; i < 16; i++) O[n][i] = 0.f;
 
         for (int tile = 0; tile < ntiles; tile++)
-            attend_tile<kRule, kPnq>(lds + tile * kStageBytes, tile, N, q, h, lane, qB0, qB1, qS0, qS1, ones,
-                                     m, lacc, O);
+            attend_tile<kRule, kPnq, 0>(lds_lane(lds + tile * kStageBytes, q, h, lane), tile, N, h, qB0, qB1,
+                                        qS0, qS1, ones, m, lacc, O);
 
         store_rows<kPnq>(a, rowbase, qi, h, lacc, O);
     }
