@@ -80,7 +80,7 @@ typedef enum {
 typedef enum {
     MXATTN_OK = 0,
     MXATTN_ERR_NULL = 1,        /* a required pointer is NULL              */
-    MXATTN_ERR_SHAPE = 2,       /* B, H or N < 1, or a size overflows       */
+    MXATTN_ERR_SHAPE = 2,       /* B, H or N < 1, or beyond a size limit    */
     MXATTN_ERR_ALIGN = 3,       /* a pointer is not 16-byte aligned         */
     MXATTN_ERR_MODE = 4,        /* mode is not an mxattn_mode value         */
     MXATTN_ERR_AXIS = 5,        /* block_axis is not 2 or 3                 */
@@ -198,8 +198,11 @@ int mxattn_attention_rowsum_diag(const void* q, const void* k, int64_t B, int64_
  * 0.53 bytes per element of each of Q, K, V), then runs the fused kernel.
  *   q, k, v  device bf16 [B, H, N, d], 16-byte aligned
  *   out      device bf16 [B, H, N, d], 16-byte aligned, must not alias inputs
+ * Size limits (MXATTN_ERR_SHAPE otherwise): N <= 2^24 keys (the kernel
+ * addresses one head's quantized K and V with 32-bit byte offsets) and
+ * B * H * ceil(N / 128) <= 2^30 query tiles.
  * Returns MXATTN_OK, MXATTN_ERR_OOM if the workspace cannot be allocated, or
- * another error status. */
+ * another error status; nothing is launched on an argument error. */
 int mxattn_forward(const void* q, const void* k, const void* v, void* out, int64_t B, int64_t H,
                    int64_t N, int64_t d, int mode, void* stream);
 
@@ -219,7 +222,7 @@ int mxattn_attend(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t
  * k and v are [B, H, Nkv, d]; the quantized variants take Q^ blocked along d
  * with Nq rows, K^ blocked along d with Nkv rows and V^ blocked along Nkv.
  * Otherwise as mxattn_forward / mxattn_attend, which are these calls with
- * Nq = Nkv = N. */
+ * Nq = Nkv = N; the key limit N <= 2^24 applies to Nkv. */
 int mxattn_cross_forward(const void* q, const void* k, const void* v, void* out, int64_t B,
                          int64_t H, int64_t Nq, int64_t Nkv, int64_t d, int mode, void* stream);
 int mxattn_cross_attend(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,

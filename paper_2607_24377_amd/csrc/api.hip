@@ -254,6 +254,14 @@ int mxattn_attention_rowsum_diag(const void* q, const void* k, int64_t B, int64_
     return MXATTN_OK;
 }
 
+// Limits of the fused attention kernel beyond check_shape: the key length
+// (32-bit byte offsets within one head's K^/V^) and the workgroup count.
+int check_attention_shape(int64_t B, int64_t H, int64_t Nq, int64_t Nkv) {
+    if (Nkv > mxattn::kMaxKeys) return MXATTN_ERR_SHAPE;
+    if (B * H * ((Nq + mxattn::kQueryTile - 1) / mxattn::kQueryTile) > (int64_t)1 << 30) return MXATTN_ERR_SHAPE;
+    return MXATTN_OK;
+}
+
 // Rearranges the K^/V^ scales into sc (mxattn::tile_scales_bytes(B*H, Nkv)
 // bytes of workspace), then runs the fused attention kernel.
 static int launch_attend(const uint8_t* qc, const uint8_t* qs, const uint8_t* kc,
@@ -278,7 +286,6 @@ static int launch_attend(const uint8_t* qc, const uint8_t* qs, const uint8_t* kc
     a.Nq = (int)Nq;
     a.nb = (int)((Nkv + 31) / 32);
     a.qtiles = (int)((Nq + mxattn::kQueryTile - 1) / mxattn::kQueryTile);
-    if (B * H * a.qtiles > (int64_t)1 << 30) return MXATTN_ERR_SHAPE;
     // one query tile per workgroup; with K^/V^ resident in LDS, as many as
     // keep about 1024 workgroups (4 per CU) busy, at most 16
     int64_t qpw = 1;
@@ -308,6 +315,7 @@ int mxattn_cross_attend(const uint8_t* q_codes, const uint8_t* q_scales, const u
     if (!valid_mode(mode)) return MXATTN_ERR_MODE;
     if (int st = check_shape(B, H, Nq, d)) return st;
     if (int st = check_shape(B, H, Nkv, d)) return st;
+    if (int st = check_attention_shape(B, H, Nq, Nkv)) return st;
     if (!aligned(q_codes, 16) || !aligned(k_codes, 16) || !aligned(v_codes, 16) ||
         !aligned(out, 16) || !aligned(k_scales, 4))
         return MXATTN_ERR_ALIGN;
@@ -342,6 +350,7 @@ int mxattn_cross_forward(const void* q, const void* k, const void* v, void* out,
     if (!valid_mode(mode)) return MXATTN_ERR_MODE;
     if (int st = check_shape(B, H, Nq, d)) return st;
     if (int st = check_shape(B, H, Nkv, d)) return st;
+    if (int st = check_attention_shape(B, H, Nq, Nkv)) return st;
     if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16))
         return MXATTN_ERR_ALIGN;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);

@@ -53,6 +53,12 @@ struct AttnArgs {
     int nchunks;        // resident kernel: workgroups per (batch, head)
 };
 
+// Largest key (and value) length of the fused attention kernel: one head's
+// K^ codes (64 B per key) and V^ codes (128 channels x 16 B per 32 keys) are
+// addressed through buffer resources with 32-bit byte offsets, which stay
+// below 2^31 up to this length.
+constexpr int64_t kMaxKeys = (int64_t)1 << 24;
+
 // Keys up to which the whole of K^ and V^ of a head stays in LDS for the
 // workgroup's lifetime (launch_attention then runs the resident kernel).
 constexpr int kResidentKeys = 512;

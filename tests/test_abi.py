@@ -93,8 +93,14 @@ def test_forward_and_attend_reject_bad_arguments(L):
     assert c(FAKE, FAKE, FAKE, FAKE, 1, 1, 0, 8, 128, 2, None) == 2    # Nq < 1
     assert c(FAKE, None, FAKE, FAKE, 1, 1, 8, 8, 128, 2, None) == 1
     assert c(FAKE, FAKE, FAKE, FAKE, 1, 1, 8, 8, 128, 5, None) == 4
+    # the fused kernel's key limit (2^24) and query-tile count (2^30), checked
+    # before any allocation or launch (the quantizer alone accepts N up to 2^28)
+    assert c(FAKE, FAKE, FAKE, FAKE, 1, 1, 8, (1 << 24) + 1, 128, 2, None) == 2
+    assert f(FAKE, FAKE, FAKE, FAKE, 1, 1, (1 << 24) + 1, 128, 2, None) == 2
+    assert c(FAKE, FAKE, FAKE, FAKE, 1 << 10, 1 << 10, (1 << 17) + 1, 8, 128, 2, None) == 2
     ca = L.mxattn_cross_attend
     assert ca(*([FAKE] * 7), 1, 1, 8, 1 << 29, 128, 2, None) == 2
+    assert ca(*([FAKE] * 7), 1, 1, 8, (1 << 24) + 1, 128, 2, None) == 2
     assert ca(*([FAKE] * 7), 1, 1, 8, 8, 64, 2, None) == 6
     a = L.mxattn_attend
     args = [FAKE] * 7
