@@ -17,7 +17,7 @@
 //      P^ = Q*(P~));
 //   5. l = alpha*l + sum(P~) (direct placement, Eq. direct_mxfp4_tile) or
 //      l = alpha*l + sum(P^) (PNQ, Eq. pnq_online_update);  the PNQ row sum
-//      of the dequantized P^ is taken on the matrix cores as ones * P^T;
+//      of the dequantized P^ is accumulated on the matrix cores (RowSum);
 //   6. O~^T = diag(alpha) O~^T + V^T P^T on the FP4 matrix cores, one
 //      64-key chunk at a time, so the first chunk's products run while the
 //      second chunk's P~ is formed.
@@ -232,6 +232,40 @@ __device__ __forceinline__ v16f mfma_fp4(v8i a, v8i b, v16f c, int sa, int sb) {
     return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 4, 4, kScaleOpsel, sa, 0, sb);
 }
 
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// 16x16x128 FP4 product with E8M0 block scales: lane l supplies row (A) or
+// column (B) l % 16 for the 32 K-values 32 (l / 16) ... 32 (l / 16) + 31
+// and their scale; D row 4 (l / 16) + i, column l % 16 is accumulator i.
+__device__ __forceinline__ v4f mfma16_fp4(v8i a, v8i b, v4f c, int sa, int sb) {
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 4, 4, 0, sa, 0, sb);
+}
+
+// The row sum l.  Direct placement: l is this lane's half of its row's sum
+// of P~ (the two halves are added at the end).  PNQ: L accumulates the sum of
+// the dequantized P^ on the matrix cores.  Read as a 16x16x128 B operand, the
+// P^ registers of a 64-key chunk hold, for column n, K-groups 0..3 = query n
+// keys 0-31, query n+16 keys 0-31, query n keys 32-63, query n+16 keys 32-63;
+// with FP4 1.0 in row 0 at K-groups 0 and 2 and in row 1 at K-groups 1 and 3
+// (row_sum_selector), D row 0 / row 1 of column n is the chunk's sum for
+// query n / n + 16.  So lanes 0-15 hold the row sums of the wave's queries
+// q (L[0]) and q + 16 (L[1]); L of the other lanes stays 0.
+struct RowSum {
+    float l;
+    v4f L;
+};
+
+// The A operand of that product: FP4 1.0 (code 0b0010) in every position of
+// row 0 at K-groups 0 and 2 and of row 1 at K-groups 1 and 3, zero elsewhere.
+__device__ __forceinline__ v8i row_sum_selector(int lane) {
+    const int row = lane & 15, group = lane >> 4;
+    const bool one = (row == 0 && (group & 1) == 0) || (row == 1 && (group & 1) == 1);
+    v8i r;
+#pragma unroll
+    for (int i = 0; i < 8; i++) r[i] = (one && i < 4) ? 0x22222222 : 0;
+    return r;
+}
+
 __device__ __forceinline__ uint32_t cvt_fp4x2(uint32_t old, float a, float b, float scale, int sel) {
     switch (sel) {
         case 0: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, a, b, scale, 0);
@@ -258,7 +292,7 @@ __device__ __forceinline__ LdsLane lds_lane(const uint8_t* st, int q, int h, int
 template <int kRule, bool kPnq, int kStage>
 __device__ __forceinline__ void attend_tile(const LdsLane& la, int tile, int N, int h,
                                             const v8i& qB0, const v8i& qB1, int qS0, int qS1,
-                                            const v8i& ones, float& m, float& lacc, v16f (&O)[4]) {
+                                            const v8i& sel, float& m, RowSum& rs, v16f (&O)[4]) {
     const float cl = 0.12751743082459868f;  // fp32(log2(e) / sqrt(128))
     constexpr int so = kStage * kStageBytes;
     const uint32_t a_sc = la.sc, a_lo = la.lo, a_hi = la.hi;
@@ -361,11 +395,17 @@ __device__ __forceinline__ void attend_tile(const LdsLane& la, int tile, int N, 
         for (int n = 0; n < 4; n++)
 #pragma unroll
             for (int i = 0; i < 16; i++) O[n][i] *= alpha;
+        if (kPnq) {
+            // lane q < 16 holds the sums of queries q and q + 16: the second
+            // takes alpha of lane q + 16 (row 1 of the first operand swaps
+            // with row 0 of the second)
+            const uint32_t ab = __builtin_bit_cast(uint32_t, alpha);
+            const auto r = __builtin_amdgcn_permlane16_swap(ab, ab, false, false);
+            rs.L[0] *= alpha;
+            rs.L[1] *= __builtin_bit_cast(float, (uint32_t)r[1]);
+        }
     }
     float lsum = 0.f;
-    v16f lt;
-#pragma unroll
-    for (int i = 0; i < 16; i++) lt[i] = 0.f;
 #pragma unroll
     for (int c = 0; c < 2; c++) {
         const float mb = __builtin_amdgcn_exp2f(__builtin_fmaf(bmax[c], cl, -m_new));
@@ -383,7 +423,7 @@ __device__ __forceinline__ void attend_tile(const LdsLane& la, int tile, int N, 
             w[n >> 3] = cvt_fp4x2(prev, p0, p1, sf, (n & 7) >> 1);
         }
         const v8i P = fp4_operand(make_uint4(w[0], w[1], w[2], w[3]));
-        if (kPnq) lt = mfma_fp4<0>(ones, P, lt, 127, psc);
+        if (kPnq) rs.L = mfma16_fp4(sel, P, rs.L, 127, psc);
         // scale byte 2 (n & 1) + c of the register of channel rows 32 n
         if (c == 0) {
             O[0] = mfma_fp4<0>(vop[0][0], P, O[0], (int)vsb.x, psc);
@@ -397,7 +437,7 @@ __device__ __forceinline__ void attend_tile(const LdsLane& la, int tile, int N, 
             O[3] = mfma_fp4<3>(vop[3][1], P, O[3], (int)vsb.y, psc);
         }
     }
-    lacc = alpha * lacc + (kPnq ? lt[0] : lsum);  // direct: this lane's half of the row
+    if (!kPnq) rs.l = alpha * rs.l + lsum;
 }
 
 // O = O~ / l rounded to bf16 (Eq. online_attention_output), as O~ times the
@@ -406,10 +446,16 @@ __device__ __forceinline__ void attend_tile(const LdsLane& la, int tile, int N, 
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 template <bool kPnq>
-__device__ __forceinline__ void store_rows(const AttnArgs& a, int64_t rowbase, int qi, int h, float lacc,
-                                           const v16f (&O)[4]) {
-    float ltot = lacc;
-    if (!kPnq) ltot += __shfl_xor(lacc, 32);
+__device__ __forceinline__ void store_rows(const AttnArgs& a, int64_t rowbase, int qi, int q, int h,
+                                           const RowSum& rs, const v16f (&O)[4]) {
+    float ltot;
+    if (kPnq) {
+        // the sums of queries q and q + 16 sit in lane q & 15 (RowSum)
+        const float l0 = __shfl(rs.L[0], q & 15), l1 = __shfl(rs.L[1], q & 15);
+        ltot = q < 16 ? l0 : l1;
+    } else {
+        ltot = rs.l + __shfl_xor(rs.l, 32);
+    }
     const float inv = 1.0f / ltot;  // one division, then 64 products
     if (qi < a.Nq) {
         uint16_t* orow = a.out + (int64_t)(rowbase + qi) * 128;
@@ -462,16 +508,12 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
     const int qS0 = a.qs[(rowbase + qic) * 4 + h];
     const int qS1 = a.qs[(rowbase + qic) * 4 + 2 + h];
 
-    // FP4 1.0 (code 0b0010) in every position: ones * P^T gives the row sums
-    // (opaque to the compiler, so it stays in VGPRs rather than being copied
-    // from scalar registers every tile)
-    v8i ones;
-#pragma unroll
-    for (int i = 0; i < 8; i++) ones[i] = i < 4 ? 0x22222222 : 0;
-    asm volatile("" : "+v"(ones));
+    const v8i sel = row_sum_selector(lane);
 
     float m = -__builtin_inff();
-    float lacc = 0.f;
+    RowSum rs;
+    rs.l = 0.f;
+    rs.L = v4f{0.f, 0.f, 0.f, 0.f};
     v16f O[4];
 #pragma unroll
     for (int n = 0; n < 4; n++)
@@ -486,19 +528,19 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
     const LdsLane la = lds_lane(lds, q, h, lane);
     for (int tile = 0;; tile += 2) {
         if (tile + 1 < ntiles) loader.load(lds + kStageBytes, tile + 1);
-        attend_tile<kRule, kPnq, 0>(la, tile, N, h, qB0, qB1, qS0, qS1, ones, m, lacc, O);
+        attend_tile<kRule, kPnq, 0>(la, tile, N, h, qB0, qB1, qS0, qS1, sel, m, rs, O);
         __builtin_amdgcn_s_waitcnt(0);  // the next tile's direct LDS loads landed
         __syncthreads();
         if (tile + 1 >= ntiles) break;
 
         if (tile + 2 < ntiles) loader.load(lds, tile + 2);
-        attend_tile<kRule, kPnq, 1>(la, tile + 1, N, h, qB0, qB1, qS0, qS1, ones, m, lacc, O);
+        attend_tile<kRule, kPnq, 1>(la, tile + 1, N, h, qB0, qB1, qS0, qS1, sel, m, rs, O);
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
         if (tile + 2 >= ntiles) break;
     }
 
-    store_rows<kPnq>(a, rowbase, qi, h, lacc, O);
+    store_rows<kPnq>(a, rowbase, qi, q, h, rs, O);
 }
 
 // Short key sequences (cross-attention over a text context, at most
@@ -531,9 +573,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_resident_kernel(AttnArg
     const TileLoader loader(a, bh, wave, lane);
     for (int t = 0; t < ntiles; t++) loader.load(lds + t * kStageBytes, t);
 
-    v8i ones;
-#pragma unroll
-    for (int i = 0; i < 8; i++) ones[i] = i < 4 ? 0x22222222 : 0;
+    const v8i sel = row_sum_selector(lane);
 
     __builtin_amdgcn_s_waitcnt(0);  // this wave's direct LDS loads landed
     __syncthreads();                // and every other wave's
@@ -562,7 +602,9 @@ __global__ __launch_bounds__(kThreads, 2) void attention_resident_kernel(AttnArg
         }
 
         float m = -__builtin_inff();
-        float lacc = 0.f;
+        RowSum rs;
+        rs.l = 0.f;
+        rs.L = v4f{0.f, 0.f, 0.f, 0.f};
         v16f O[4];
 #pragma unroll
         for (int n = 0; n < 4; n++)
@@ -571,9 +613,9 @@ __global__ __launch_bounds__(kThreads, 2) void attention_resident_kernel(AttnArg
 
         for (int tile = 0; tile < ntiles; tile++)
             attend_tile<kRule, kPnq, 0>(lds_lane(lds + tile * kStageBytes, q, h, lane), tile, N, h, qB0, qB1,
-                                        qS0, qS1, ones, m, lacc, O);
+                                        qS0, qS1, sel, m, rs, O);
 
-        store_rows<kPnq>(a, rowbase, qi, h, lacc, O);
+        store_rows<kPnq>(a, rowbase, qi, q, h, rs, O);
     }
 }
 
