@@ -117,7 +117,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-overhead", action="store_true")
     ap.add_argument("--no-next", action="store_true",
-                    help="skip the boundary-sweep timings (the scope table's next rows)")
+                    help="skip the boundary-sweep and row-sum diagnostic timings")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
