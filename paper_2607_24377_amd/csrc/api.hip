@@ -31,11 +31,14 @@ bool valid_mode(int mode) { return mode >= MXATTN_OCP_VANILLA && mode <= MXATTN_
 // were quantized.
 int kernel_mode(int mode) { return mode == MXATTN_UOS_PNQ_ROT ? MXATTN_UOS_PNQ : mode; }
 
-// Shape limits of the kernels: 32-bit token indices, 64-bit byte offsets.
+// Shape limits of the kernels: 32-bit token indices, 64-bit byte offsets, and
+// at most 2^35 elements per tensor (64 GiB of bf16), which keeps every grid
+// below 2^31 workgroups.
 int check_shape(int64_t B, int64_t H, int64_t N, int64_t d) {
     if (B < 1 || H < 1 || N < 1 || d < 1) return MXATTN_ERR_SHAPE;
     if (B > (1 << 20) || H > (1 << 20) || N > (1 << 28)) return MXATTN_ERR_SHAPE;
     if (B * H > (int64_t)1 << 24) return MXATTN_ERR_SHAPE;
+    if (B * H * N * 128 > (int64_t)1 << 35) return MXATTN_ERR_SHAPE;
     if (d != 128) return MXATTN_ERR_UNSUPPORTED;
     return MXATTN_OK;
 }

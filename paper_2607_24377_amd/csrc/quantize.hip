@@ -13,21 +13,24 @@
 
 namespace mxattn {
 
+// The bf16 inputs are read exactly once: non-temporal loads keep them from
+// displacing cached lines (measured ~10 % faster than ordinary loads here).
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 nt_load(const uint4* p) {
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+    return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
 // ---------------------------------------------------------------------------
-// Blocks along the head dimension (Q and K).  Each thread owns 8 consecutive
-// elements (one 16-byte load); the 4 threads of a 32-element block are
+// Blocks along the head dimension (Q and K).  A thread owns 8 consecutive
+// elements (one 16-byte chunk) in each of two grid-strided passes, both
+// loaded before either is quantized; the 4 threads of a 32-element block are
 // adjacent lanes and exchange their maxima with two lane swaps.
 // ---------------------------------------------------------------------------
+// Quantizes the 16-byte chunk v (8 elements) of chunk index i.
 template <int kRule>
-__global__ __launch_bounds__(256) void quantize_headdim_kernel(const uint4* __restrict__ x,
-                                                               uint32_t* __restrict__ codes,
-                                                               uint8_t* __restrict__ scales,
-                                                               int64_t n_chunks, Boundary bq) {
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    const bool valid = i < n_chunks;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (valid) v = x[i];
-
+__device__ __forceinline__ void quantize_chunk(uint4 v, int64_t i, bool valid, uint32_t* __restrict__ codes,
+                                               uint8_t* __restrict__ scales, Boundary bq) {
     // block maximum of |x| on the bf16 bit patterns (order-preserving for
     // nonnegative finite values)
     uint32_t m = 0;
@@ -41,11 +44,9 @@ __global__ __launch_bounds__(256) void quantize_headdim_kernel(const uint4* __re
     m = max(m, (v.w >> 16) & 0x7FFFu);
     m = max(m, (uint32_t)__shfl_xor((int)m, 1));
     m = max(m, (uint32_t)__shfl_xor((int)m, 2));
-
     // all-zero block: sigma = 1 (Algorithm 1); codes come out as signed zeros
     const uint32_t sbyte = (m == 0) ? 127u : (uint32_t)(block_exponent_bf16<kRule>(m, bq) + 127);
     const float sf = e8m0_as_f32(sbyte);
-
     uint32_t c = 0;
     c = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c, __builtin_bit_cast(bf16x2, v.x), sf, 0);
     c = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c, __builtin_bit_cast(bf16x2, v.y), sf, 1);
@@ -54,6 +55,26 @@ __global__ __launch_bounds__(256) void quantize_headdim_kernel(const uint4* __re
     if (valid) {
         codes[i] = c;
         if ((i & 3) == 0) scales[i >> 2] = (uint8_t)sbyte;
+    }
+}
+
+template <int kRule>
+__global__ __launch_bounds__(256) void quantize_headdim_kernel(const uint4* __restrict__ x,
+                                                               uint32_t* __restrict__ codes,
+                                                               uint8_t* __restrict__ scales,
+                                                               int64_t n_chunks, Boundary bq) {
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    const int64_t i0 = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    uint4 v[2];
+#pragma unroll
+    for (int k = 0; k < 2; k++) {
+        const int64_t i = i0 + k * stride;
+        v[k] = i < n_chunks ? nt_load(x + i) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int k = 0; k < 2; k++) {
+        const int64_t i = i0 + k * stride;
+        quantize_chunk<kRule>(v[k], i, i < n_chunks, codes, scales, bq);
     }
 }
 
@@ -77,7 +98,7 @@ __global__ __launch_bounds__(256) void quantize_headdim_rot_kernel(const uint4* 
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     const bool valid = i < n_chunks;
     uint4 v = make_uint4(0, 0, 0, 0);
-    if (valid) v = x[i];
+    if (valid) v = nt_load(x + i);
     const int t = threadIdx.x & 15;  // thread within the row: elements 8t..8t+7
 
     float y[8];
@@ -145,14 +166,22 @@ template <int kRule>
 __global__ __launch_bounds__(256) void quantize_tokens_kernel(const uint4* __restrict__ x,
                                                               uint8_t* __restrict__ codes,
                                                               uint8_t* __restrict__ scales, int N,
-                                                              int nb, int groups, Boundary bq) {
+                                                              int nb, int groups, int per_xcd, int total,
+                                                              Boundary bq) {
     // [token][64 dwords = 128 bf16]; the 32-token quarter q of the group is
     // stored with its dword columns XOR-ed by 16 q, so that the four lanes
     // reading the same channel pair in four quarters hit four bank groups
     __shared__ uint32_t tile[kVqTokens * 64];
     const int tid = threadIdx.x;
-    const int bh = blockIdx.x / groups;
-    const int g = blockIdx.x % groups;
+    // consecutive workgroup ids go round-robin over the 8 XCDs: give each XCD
+    // a contiguous range of (head, group), so that neighbouring groups, whose
+    // outputs share cache lines in every channel row, meet in one L2 and
+    // reach HBM as whole lines
+    const int L = blockIdx.x;
+    const int logical = (L & 7) * per_xcd + (L >> 3);
+    if (logical >= total) return;
+    const int bh = logical / groups;
+    const int g = logical % groups;
     const int tok0 = g * kVqTokens;
 
     const uint4* src = x + (int64_t)bh * N * 16;  // 16 chunks of 16 B per token
@@ -161,7 +190,7 @@ __global__ __launch_bounds__(256) void quantize_tokens_kernel(const uint4* __res
         int ch = tid + 256 * k;  // chunk id within the group
         int tok = ch >> 4, part = ch & 15;
         uint4 v = make_uint4(0, 0, 0, 0);
-        if (tok0 + tok < N) v = src[(int64_t)(tok0 + tok) * 16 + part];
+        if (tok0 + tok < N) v = nt_load(src + (int64_t)(tok0 + tok) * 16 + part);
         *reinterpret_cast<uint4*>(&tile[tok * 64 + ((part * 4) ^ (16 * (tok >> 5)))]) = v;
     }
     __syncthreads();
@@ -233,7 +262,7 @@ hipError_t launch_quantize_headdim(const void* x, uint8_t* codes, uint8_t* scale
                                    int rule, hipStream_t stream, double qmax) {
     const int64_t n_chunks = rows * 16;  // d = 128: 16 chunks of 8 elements per row
     if (n_chunks == 0) return hipSuccess;
-    const dim3 grid((unsigned)((n_chunks + 255) / 256));
+    const dim3 grid((unsigned)(((n_chunks + 2 - 1) / 2 + 255) / 256));
     const Boundary bq = boundary_of(rule == kRuleQmax ? qmax : 7.25);
     if (rule == kRuleUos)
         quantize_headdim_kernel<kRuleUos><<<grid, 256, 0, stream>>>(
@@ -265,17 +294,19 @@ hipError_t launch_quantize_tokens(const void* x, uint8_t* codes, uint8_t* scales
                                   int64_t N, int rule, hipStream_t stream, double qmax) {
     const int nb = (int)((N + 31) / 32);
     const int groups = (int)((N + kVqTokens - 1) / kVqTokens);
-    const dim3 grid((unsigned)(BH * groups));
+    const int total = (int)(BH * groups);
+    const int per_xcd = (total + 7) / 8;
+    const dim3 grid((unsigned)(8 * per_xcd));
     const Boundary bq = boundary_of(rule == kRuleQmax ? qmax : 7.25);
     if (rule == kRuleUos)
         quantize_tokens_kernel<kRuleUos><<<grid, 256, 0, stream>>>((const uint4*)x, codes, scales,
-                                                                    (int)N, nb, groups, bq);
+                                                                    (int)N, nb, groups, per_xcd, total, bq);
     else if (rule == kRuleQmax)
         quantize_tokens_kernel<kRuleQmax><<<grid, 256, 0, stream>>>((const uint4*)x, codes, scales,
-                                                                     (int)N, nb, groups, bq);
+                                                                     (int)N, nb, groups, per_xcd, total, bq);
     else
         quantize_tokens_kernel<kRuleOcp><<<grid, 256, 0, stream>>>((const uint4*)x, codes, scales,
-                                                                    (int)N, nb, groups, bq);
+                                                                    (int)N, nb, groups, per_xcd, total, bq);
     return hipGetLastError();
 }
 

@@ -79,6 +79,15 @@ def test_quantize_rejects_bad_arguments(L):
     assert q(FAKE, FAKE + 8, FAKE, 3, 2, 1, 1, 8, 128, None) == 3
 
 
+def test_element_count_limit(L):
+    """At most 2^35 elements per tensor (every grid stays below 2^31
+    workgroups); the byte-size queries return 0 beyond it."""
+    q = L.mxattn_quantize
+    assert q(FAKE, FAKE, FAKE, 3, 2, 1 << 8, 1 << 8, 1 << 20, 128, None) == 2
+    assert L.mxattn_codes_bytes(3, 1 << 8, 1 << 8, 1 << 20, 128) == 0
+    assert L.mxattn_codes_bytes(3, 1 << 8, 1 << 8, 1 << 12, 128) == (1 << 28) * 64
+
+
 def test_forward_and_attend_reject_bad_arguments(L):
     f = L.mxattn_forward
     assert f(None, FAKE, FAKE, FAKE, 1, 1, 8, 128, 2, None) == 1
