@@ -68,17 +68,7 @@ constexpr int kStageBytes = 17408;
 // the same logical slot hit 16 distinct 16-byte bank groups.
 __device__ __forceinline__ int swz(int row) { return ((row >> 1) ^ (row >> 2)) & 3; }
 
-// Row of the K^ tile (in MFMA order) that holds key w (0..63) of a 64-key
-// chunk: tile j = bit 4 of w, A-row r = 8*(w bits 2-3) + 4*(w bit 5) + (w & 3).
-// In the 32x32 output layout, accumulator i of lane (q, h) is A-row
-// 8*(i/4) + 4*h + (i%4), so lane (q, h) receives key 32*h + 16*j + i.
-__device__ __forceinline__ void key_slot(int w, int& j, int& r) {
-    j = (w >> 4) & 1;
-    r = 8 * ((w >> 2) & 3) + 4 * ((w >> 5) & 1) + (w & 3);
-}
-
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
-typedef __attribute__((address_space(1))) void* gbl_ptr_t;
 
 // Global -> LDS copy of one tile's K^ and V^ codes (16 KiB) with the direct
 // gfx950 LDS loads: lane i of a wave-wide load writes the 16 bytes it fetched
@@ -116,8 +106,14 @@ struct TileLoader {
         for (int it = 0; it < 2; it++) {
             const int p = (2 * wave + it) * 64 + lane;  // 16-byte slot of the region
             const int row = p >> 2;
-            // K^: row -> (chunk c, tile j, A-row r) -> key; slot -> channel
-            // block.  V^: row = channel, slot -> key block (same swizzle).
+            // K^: LDS row 64 c + 32 j + r is A-row r of the S product for
+            // 32-key tile j of 64-key chunk c, and holds key
+            // 64 c + 32 ((r >> 2) & 1) + 16 j + 4 (r >> 3) + (r & 3).  In the
+            // 32x32 output layout accumulator i of lane (q, h) is A-row
+            // 8 (i / 4) + 4 h + (i % 4), so after both tiles of a chunk lane
+            // (q, h) holds keys 32 h .. 32 h + 31 of the chunk in order.  The
+            // slot is the channel block.  V^: row = channel, slot -> key block
+            // (same swizzle).
             const int r = row & 31, j = (row >> 5) & 1, c = row >> 6;
             const int key = 64 * c + 32 * ((r >> 2) & 1) + 16 * j + 4 * (r >> 3) + (r & 3);
             const int db = (p & 3) ^ swz(row);
