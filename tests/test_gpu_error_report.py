@@ -38,7 +38,7 @@ def mx():
     return mxattn
 
 
-@pytest.mark.parametrize("cfg", [0, 1, 2])
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
 def test_modes_against_exact_attention(mx, cfg):
     w = inputs.workload(cfg)
     q, k, v = workload_bits(cfg)
