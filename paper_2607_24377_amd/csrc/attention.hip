@@ -34,10 +34,11 @@
 // quantization and the B-operand layout of the 32x32x64 PV product.
 //
 // The softmax path (one FMA, one exp, half an FP4 conversion and half a
-// 3-way max per score) costs several times the matrix-core time of the two
-// products, so the kernel is VALU-bound; two workgroups per CU give each SIMD
-// two waves, and the matrix-core work of one hides under the softmax of the
-// other.
+// 3-way max per score) costs about twice the matrix-core time of the two
+// products, so the kernel is bound by vector-ALU issue; two workgroups per CU
+// give each SIMD two waves, whose matrix-core work overlaps the other's
+// softmax (not for free: vector instructions issue 30-45 % slower while an
+// FP4 MFMA executes).
 //
 // Arithmetic contract (mirrored by the CPU oracle):
 //   s     fp32 accumulation of exact FP4 products (matrix core)
@@ -70,19 +71,21 @@ __device__ __forceinline__ int swz(int row) { return ((row >> 1) ^ (row >> 2)) &
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
-// Global -> LDS copy of one tile's K^ and V^ codes (16 KiB) with the direct
-// gfx950 LDS loads: lane i of a wave-wide load writes the 16 bytes it fetched
-// to LDS base + 16*i, so each lane fetches whatever chunk belongs at its slot
-// of the permuted, swizzled layout.  Nothing passes through VGPRs; completion
-// is tracked by vmcnt.  Wave w copies LDS bytes [2048 w, 2048 w + 2048) of
-// each of the two 8 KiB code regions, and wave 0 also the tile's K^ and V^
-// scales, already in the lanes' MFMA operand order (tile_scales_kernel).
-// Each source is a buffer resource over one head's array: a lane's offset
-// within a tile is fixed, the tile's offset is a scalar, so no per-tile
-// address arithmetic runs on the vector units.  Bytes past the end of an
-// array read as zero (buffer range check): the K^ rows of keys past N (their
-// scores are masked) and the V^ key blocks past the end (the matching P^
-// entries are zero) contribute nothing.
+// Global -> LDS copy of one tile's K^ and V^ codes (16 KiB) with gfx950
+// buffer loads that write to LDS: lane i of a wave-wide load writes the 16
+// bytes it fetched to LDS base + 16*i, so each lane fetches whatever chunk
+// belongs at its slot of the permuted, swizzled layout.  Nothing passes
+// through VGPRs; completion is tracked by vmcnt.  Wave w copies LDS bytes
+// [2048 w, 2048 w + 2048) of each of the two 8 KiB code regions, and wave 0
+// also the tile's K^ and V^ scales, already in the lanes' MFMA operand order
+// (tile_scales_kernel).  Each source is a buffer resource over one head's
+// array: a lane's offset within a tile is fixed, the tile's offset is a
+// scalar, so no per-tile address arithmetic runs on the vector units.  In the
+// last tile, K^ rows of keys past N lie past the end of the head's array and
+// read as zero (buffer range check; their scores are masked anyway); V^ key
+// blocks past the end of a channel row read the start of the next row (zeros
+// after the last row).  Those V^ values meet P^ entries that are zero, and
+// FP4 codes and E8M0 scales are always finite, so they contribute nothing.
 struct TileLoader {
     __amdgpu_buffer_rsrc_t kc;  // this head's K^ codes [N, 64]
     __amdgpu_buffer_rsrc_t vc;  // this head's V^ codes [128, nb * 16]
@@ -187,9 +190,10 @@ __device__ __forceinline__ uint32_t p_scale_byte(uint32_t mbits) {
 }
 
 // LDS reads issued as inline assembly.  The compiler does not see them as LDS
-// accesses, so it does not make them wait for the direct global->LDS loads
-// of the next tile (which it cannot tell apart from the stage being read);
-// completion is awaited explicitly with lds_wait().
+// accesses, so it does not make them wait for the buffer-to-LDS loads of the
+// next tile (which it cannot tell apart from the stage being read); the reads'
+// completion is awaited by explicit s_waitcnt lgkmcnt statements that name
+// the destination registers.
 typedef int v4i __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
     return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
