@@ -93,12 +93,4 @@ __device__ __forceinline__ v8i fp4_operand(uint4 v) {
     return r;
 }
 
-// Largest fp32 strictly below x (x finite).
-__device__ __forceinline__ float next_down(float x) {
-    uint32_t u = __builtin_bit_cast(uint32_t, x);
-    if (x > 0.f) return __builtin_bit_cast(float, u - 1u);
-    if (x < 0.f) return __builtin_bit_cast(float, u + 1u);
-    return -1.40129846e-45f;
-}
-
 }  // namespace mxattn
