@@ -193,9 +193,13 @@ int mxattn_attention_rowsum_diag(const void* q, const void* k, int64_t B, int64_
 
 /* MXFP4 attention forward O = softmax(Q K^T / sqrt(d)) V with MXFP4 Q, K, V
  * and MXFP4 P~ (Algorithm 2, with its Hadamard rotation in mode
- * MXATTN_UOS_PNQ_ROT only; non-causal, no mask besides the sequence end).  Quantizes Q and K along d and V along N into
- * stream-ordered workspace (hipMallocAsync/hipFreeAsync on `stream`, about
- * 0.53 bytes per element of each of Q, K, V), then runs the fused kernel.
+ * MXATTN_UOS_PNQ_ROT only; non-causal, no mask besides the sequence end).
+ * Quantizes K along d and V along N into stream-ordered workspace
+ * (hipMallocAsync/hipFreeAsync on `stream`, about 0.53 bytes per element of
+ * each of K and V), then runs the fused kernel, which quantizes Q along d in
+ * its prologue with codes bit-identical to mxattn_quantize's; in
+ * MXATTN_UOS_PNQ_ROT, Q is rotated and quantized into the workspace first
+ * (0.53 bytes per element more).
  *   q, k, v  device bf16 [B, H, N, d], 16-byte aligned
  *   out      device bf16 [B, H, N, d], 16-byte aligned, must not alias inputs
  * Size limits (MXATTN_ERR_SHAPE otherwise): N <= 2^24 keys (the kernel

@@ -266,8 +266,10 @@ int check_attention_shape(int64_t B, int64_t H, int64_t Nq, int64_t Nkv) {
 }
 
 // Rearranges the K^/V^ scales into sc (mxattn::tile_scales_bytes(B*H, Nkv)
-// bytes of workspace), then runs the fused attention kernel.
-static int launch_attend(const uint8_t* qc, const uint8_t* qs, const uint8_t* kc,
+// bytes of workspace), then runs the fused attention kernel: on Q^ = (qc, qs),
+// or, when qraw is not null, on the bf16 Q that the kernel quantizes itself
+// (qc and qs are then unused).
+static int launch_attend(const void* qraw, const uint8_t* qc, const uint8_t* qs, const uint8_t* kc,
                          const uint8_t* ks, const uint8_t* vc, const uint8_t* vs, uint8_t* sc,
                          void* out, int64_t B, int64_t H, int64_t Nq, int64_t Nkv, int mode,
                          hipStream_t s) {
@@ -279,6 +281,7 @@ static int launch_attend(const uint8_t* qc, const uint8_t* qs, const uint8_t* kc
     mxattn::AttnArgs a;
     a.qc = qc;
     a.qs = qs;
+    a.qraw = static_cast<const uint16_t*>(qraw);
     a.kc = kc;
     a.ks = ks;
     a.vc = vc;
@@ -330,7 +333,7 @@ int mxattn_cross_attend(const uint8_t* q_codes, const uint8_t* q_scales, const u
         set_error("hipMallocAsync", e);
         return MXATTN_ERR_OOM;
     }
-    int st = launch_attend(q_codes, q_scales, k_codes, k_scales, v_codes, v_scales,
+    int st = launch_attend(nullptr, q_codes, q_scales, k_codes, k_scales, v_codes, v_scales,
                            static_cast<uint8_t*>(ws), out, B, H, Nq, Nkv, mode, s);
     e = hipFreeAsync(ws, s);
     if (st == MXATTN_OK && e != hipSuccess) {
@@ -359,8 +362,12 @@ int mxattn_cross_forward(const void* q, const void* k, const void* v, void* out,
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     keep_pool_memory();
 
-    const size_t q_codes = mxattn_codes_bytes(MXATTN_AXIS_HEAD_DIM, B, H, Nq, d);
-    const size_t q_scales = mxattn_scales_bytes(MXATTN_AXIS_HEAD_DIM, B, H, Nq, d);
+    // Q is quantized in the attention kernel's prologue (bit-identical to the
+    // head-dim quantizer), except for the rotated mode, whose Q is rotated
+    // across all 128 channels first by its own quantizer
+    const bool q_fused = mode != MXATTN_UOS_PNQ_ROT;
+    const size_t q_codes = q_fused ? 0 : mxattn_codes_bytes(MXATTN_AXIS_HEAD_DIM, B, H, Nq, d);
+    const size_t q_scales = q_fused ? 0 : mxattn_scales_bytes(MXATTN_AXIS_HEAD_DIM, B, H, Nq, d);
     const size_t k_codes = mxattn_codes_bytes(MXATTN_AXIS_HEAD_DIM, B, H, Nkv, d);
     const size_t k_scales = mxattn_scales_bytes(MXATTN_AXIS_HEAD_DIM, B, H, Nkv, d);
     const size_t v_codes = mxattn_codes_bytes(MXATTN_AXIS_TOKENS, B, H, Nkv, d);
@@ -397,13 +404,13 @@ int mxattn_cross_forward(const void* q, const void* k, const void* v, void* out,
         return mode == MXATTN_UOS_PNQ_ROT ? mxattn::launch_quantize_headdim_rotated(x, c, sc, rows, rule, st)
                                           : mxattn::launch_quantize_headdim(x, c, sc, rows, rule, st);
     };
-    if ((e = qk(q, qc, qs, B * H * Nq, rule, s)) != hipSuccess ||
+    if ((!q_fused && (e = qk(q, qc, qs, B * H * Nq, rule, s)) != hipSuccess) ||
         (e = qk(k, kc, ks, B * H * Nkv, rule, s)) != hipSuccess ||
         (e = mxattn::launch_quantize_tokens(v, vc, vs, B * H, Nkv, rule, s)) != hipSuccess) {
         set_error("quantize launch", e);
         st = MXATTN_ERR_HIP;
     } else {
-        st = launch_attend(qc, qs, kc, ks, vc, vs, sc, out, B, H, Nq, Nkv, mode, s);
+        st = launch_attend(q_fused ? q : nullptr, qc, qs, kc, ks, vc, vs, sc, out, B, H, Nq, Nkv, mode, s);
     }
     e = hipFreeAsync(ws, s);
     if (st == MXATTN_OK && e != hipSuccess) {

@@ -48,6 +48,8 @@
 //   scale from the block maximum of P~ (exp2 of the block's largest t)
 //   P^    the gfx950 FP4 conversion of P~ / 2^e (round to nearest, ties to
 //         the even code, saturating)
+#include <type_traits>
+
 #include "device_common.h"
 #include "launch.h"
 
@@ -286,15 +288,87 @@ __device__ __forceinline__ LdsLane lds_lane(const uint8_t* st, int q, int h, int
     return {base + lane * 8, base + q * 64 + 16 * ((0 + h) ^ swz(q)), base + q * 64 + 16 * ((2 + h) ^ swz(q))};
 }
 
+// The Q^ operands of S^T = K^ Q^T for one query row: lane (q, h) holds channel
+// blocks h and 2 + h of its query (the B operands of the products over
+// channels 0-63 and 64-127) and their E8M0 scales.
+struct QOperands {
+    v8i b0, b1;
+    int s0, s1;
+};
+
+// From Q^ quantized beforehand ([BH, Nq, 64] codes, [BH, Nq, 4] scales).
+__device__ __forceinline__ QOperands q_operands(const AttnArgs& a, int64_t row, int h) {
+    const uint8_t* qrow = a.qc + row * 64;
+    return {fp4_operand(*reinterpret_cast<const uint4*>(qrow + 16 * h)),
+            fp4_operand(*reinterpret_cast<const uint4*>(qrow + 16 * (2 + h))), (int)a.qs[row * 4 + h],
+            (int)a.qs[row * 4 + 2 + h]};
+}
+
+// The two bf16 channel blocks (32 values each) of a query row that lane half
+// h quantizes itself: channels 32 h .. 32 h + 31 and 64 + 32 h .. 64 + 32 h + 31.
+struct QRaw {
+    uint4 v[8];
+};
+__device__ __forceinline__ QRaw q_raw(const AttnArgs& a, int64_t row, int h) {
+    const uint4* src = reinterpret_cast<const uint4*>(a.qraw + row * 128);
+    QRaw r;
+#pragma unroll
+    for (int k = 0; k < 4; k++) {
+        r.v[k] = src[4 * h + k];
+        r.v[4 + k] = src[8 + 4 * h + k];
+    }
+    return r;
+}
+
+// One 32-value block quantized exactly as quantize_headdim_kernel does it
+// (Algorithm 1 with the mode's rule): the block maximum on the bf16
+// magnitude bits, its E8M0 exponent (an all-zero block gets sigma = 1) and
+// the gfx950 FP4 conversion, so the codes are bit-identical to that kernel's.
+template <int kRule>
+__device__ __forceinline__ v8i quantize_q_block(const uint4* v, int& sbyte) {
+    uint32_t m = 0;
+#pragma unroll
+    for (int k = 0; k < 4; k++) {
+        const uint32_t w[4] = {v[k].x, v[k].y, v[k].z, v[k].w};
+#pragma unroll
+        for (int e = 0; e < 4; e++) m = max(m, max(w[e] & 0x7FFFu, (w[e] >> 16) & 0x7FFFu));
+    }
+    const uint32_t sb = (m == 0) ? 127u : (uint32_t)(scale_exponent_bf16<kRule>(m) + 127);
+    const float sf = e8m0_as_f32(sb);
+    uint32_t c[4];
+#pragma unroll
+    for (int k = 0; k < 4; k++) {
+        uint32_t x = 0;
+        x = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(x, __builtin_bit_cast(bf16x2, v[k].x), sf, 0);
+        x = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(x, __builtin_bit_cast(bf16x2, v[k].y), sf, 1);
+        x = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(x, __builtin_bit_cast(bf16x2, v[k].z), sf, 2);
+        x = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(x, __builtin_bit_cast(bf16x2, v[k].w), sf, 3);
+        c[k] = x;
+    }
+    sbyte = (int)sb;
+    return fp4_operand(make_uint4(c[0], c[1], c[2], c[3]));
+}
+
+template <int kRule>
+__device__ __forceinline__ QOperands quantize_q(const QRaw& r) {
+    QOperands o;
+    o.b0 = quantize_q_block<kRule>(r.v, o.s0);
+    o.b1 = quantize_q_block<kRule>(r.v + 4, o.s1);
+    return o;
+}
+
 // One KV tile of Algorithm 2 for the wave's 32 query rows, on LDS stage
 // kStage (relative to la): S^T = K^ Q^T, the online-softmax update of (m, l),
 // P^ and O~^T += V^T P^T.  Reads LDS only; the caller owns loads and barriers.
 template <int kRule, bool kPnq, int kStage>
 __device__ __forceinline__ void attend_tile(const LdsLane& la, int tile, int N, int h,
-                                            const v8i& qB0, const v8i& qB1, int qS0, int qS1,
-                                            const v8i& sel, float& m, RowSum& rs, v16f (&O)[4]) {
+                                            const QOperands& qo, const v8i& sel, float& m, RowSum& rs,
+                                            v16f (&O)[4]) {
     const float cl = 0.12751743082459868f;  // fp32(log2(e) / sqrt(128))
     constexpr int so = kStage * kStageBytes;
+    const v8i& qB0 = qo.b0;
+    const v8i& qB1 = qo.b1;
+    const int qS0 = qo.s0, qS1 = qo.s1;
     const uint32_t a_sc = la.sc, a_lo = la.lo, a_hi = la.hi;
     uint2 ksb = lds_read64<so + kKsOff>(a_sc);
     uint2 vsb = lds_read64<so + kVsOff>(a_sc);
@@ -474,7 +548,7 @@ __device__ __forceinline__ void store_rows(const AttnArgs& a, int64_t rowbase, i
     }
 }
 
-template <int kRule, bool kPnq>
+template <int kRule, bool kPnq, bool kQraw>
 __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
     __shared__ __attribute__((aligned(16))) uint8_t lds[2 * kStageBytes];
     const int tid = threadIdx.x;
@@ -500,13 +574,12 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
     const TileLoader loader(a, bh, wave, lane);
     loader.load(lds, 0);
 
-    // Q^ as the B operand of S^T = K^ Q^T: lane (q, h) holds channel block
-    // 2*hf + h of its query for the product over channels 64*hf..64*hf+63.
-    const uint8_t* qrow = a.qc + (rowbase + qic) * 64;
-    const v8i qB0 = fp4_operand(*reinterpret_cast<const uint4*>(qrow + 16 * h));
-    const v8i qB1 = fp4_operand(*reinterpret_cast<const uint4*>(qrow + 16 * (2 + h)));
-    const int qS0 = a.qs[(rowbase + qic) * 4 + h];
-    const int qS1 = a.qs[(rowbase + qic) * 4 + 2 + h];
+    // Q^ as the B operand of S^T = K^ Q^T
+    QOperands qo;
+    if constexpr (kQraw)
+        qo = quantize_q<kRule>(q_raw(a, rowbase + qic, h));
+    else
+        qo = q_operands(a, rowbase + qic, h);
 
     const v8i sel = row_sum_selector(lane);
 
@@ -528,13 +601,13 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
     const LdsLane la = lds_lane(lds, q, h, lane);
     for (int tile = 0;; tile += 2) {
         if (tile + 1 < ntiles) loader.load(lds + kStageBytes, tile + 1);
-        attend_tile<kRule, kPnq, 0>(la, tile, N, h, qB0, qB1, qS0, qS1, sel, m, rs, O);
+        attend_tile<kRule, kPnq, 0>(la, tile, N, h, qo, sel, m, rs, O);
         __builtin_amdgcn_s_waitcnt(0);  // the next tile's direct LDS loads landed
         __syncthreads();
         if (tile + 1 >= ntiles) break;
 
         if (tile + 2 < ntiles) loader.load(lds, tile + 2);
-        attend_tile<kRule, kPnq, 1>(la, tile + 1, N, h, qB0, qB1, qS0, qS1, sel, m, rs, O);
+        attend_tile<kRule, kPnq, 1>(la, tile + 1, N, h, qo, sel, m, rs, O);
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
         if (tile + 2 >= ntiles) break;
@@ -550,7 +623,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
 // as in attention_kernel.
 constexpr int kResidentTiles = kResidentKeys / 128;
 
-template <int kRule, bool kPnq>
+template <int kRule, bool kPnq, bool kQraw>
 __global__ __launch_bounds__(kThreads, 2) void attention_resident_kernel(AttnArgs a) {
     __shared__ __attribute__((aligned(16))) uint8_t lds[kResidentTiles * kStageBytes];
     const int tid = threadIdx.x;
@@ -578,28 +651,26 @@ __global__ __launch_bounds__(kThreads, 2) void attention_resident_kernel(AttnArg
     __builtin_amdgcn_s_waitcnt(0);  // this wave's direct LDS loads landed
     __syncthreads();                // and every other wave's
 
-    // Q^ operands of the first query tile; each later one is loaded while
-    // the previous tile is processed
-    auto q_row = [&](int qt) { return min(qt * kQueryTile + wave * kQw + q, Nq - 1); };
-    int qic = q_row(qt0);
-    uint4 qa0 = *reinterpret_cast<const uint4*>(a.qc + (rowbase + qic) * 64 + 16 * h);
-    uint4 qa1 = *reinterpret_cast<const uint4*>(a.qc + (rowbase + qic) * 64 + 16 * (2 + h));
-    int qs0 = a.qs[(rowbase + qic) * 4 + h];
-    int qs1 = a.qs[(rowbase + qic) * 4 + 2 + h];
+    // the Q^ operands (or the bf16 rows to quantize) of the first query tile;
+    // each later one is fetched while the previous tile is processed
+    auto q_row = [&](int qt) { return rowbase + min(qt * kQueryTile + wave * kQw + q, Nq - 1); };
+    using QFetch = std::conditional_t<kQraw, QRaw, QOperands>;
+    auto fetch = [&](int qt) -> QFetch {
+        if constexpr (kQraw)
+            return q_raw(a, q_row(qt), h);
+        else
+            return q_operands(a, q_row(qt), h);
+    };
+    QFetch next = fetch(qt0);
 
     for (int qt = qt0; qt < qt1; qt++) {
         const int qi = qt * kQueryTile + wave * kQw + q;
-        const v8i qB0 = fp4_operand(qa0);
-        const v8i qB1 = fp4_operand(qa1);
-        const int qS0 = qs0;
-        const int qS1 = qs1;
-        if (qt + 1 < qt1) {
-            qic = q_row(qt + 1);
-            qa0 = *reinterpret_cast<const uint4*>(a.qc + (rowbase + qic) * 64 + 16 * h);
-            qa1 = *reinterpret_cast<const uint4*>(a.qc + (rowbase + qic) * 64 + 16 * (2 + h));
-            qs0 = a.qs[(rowbase + qic) * 4 + h];
-            qs1 = a.qs[(rowbase + qic) * 4 + 2 + h];
-        }
+        QOperands qo;
+        if constexpr (kQraw)
+            qo = quantize_q<kRule>(next);
+        else
+            qo = next;
+        if (qt + 1 < qt1) next = fetch(qt + 1);
 
         float m = -__builtin_inff();
         RowSum rs;
@@ -612,8 +683,8 @@ __global__ __launch_bounds__(kThreads, 2) void attention_resident_kernel(AttnArg
             for (int i = 0; i < 16; i++) O[n][i] = 0.f;
 
         for (int tile = 0; tile < ntiles; tile++)
-            attend_tile<kRule, kPnq, 0>(lds_lane(lds + tile * kStageBytes, q, h, lane), tile, N, h, qB0, qB1,
-                                        qS0, qS1, sel, m, rs, O);
+            attend_tile<kRule, kPnq, 0>(lds_lane(lds + tile * kStageBytes, q, h, lane), tile, N, h, qo, sel, m,
+                                        rs, O);
 
         store_rows<kPnq>(a, rowbase, qi, q, h, rs, O);
     }
@@ -670,21 +741,29 @@ hipError_t launch_tile_scales(const uint8_t* ks, const uint8_t* vs, uint8_t* out
     return hipGetLastError();
 }
 
-hipError_t launch_attention(const AttnArgs& a, int mode, hipStream_t stream) {
-    const dim3 grid((unsigned)(8 * a.per_xcd));
+template <bool kQraw>
+static void launch_attention_q(const AttnArgs& a, int mode, dim3 grid, hipStream_t stream) {
     if (a.N <= kResidentKeys) {
         switch (mode) {
-            case 0: attention_resident_kernel<kRuleOcp, false><<<grid, kThreads, 0, stream>>>(a); break;
-            case 1: attention_resident_kernel<kRuleUos, false><<<grid, kThreads, 0, stream>>>(a); break;
-            default: attention_resident_kernel<kRuleUos, true><<<grid, kThreads, 0, stream>>>(a); break;
+            case 0: attention_resident_kernel<kRuleOcp, false, kQraw><<<grid, kThreads, 0, stream>>>(a); break;
+            case 1: attention_resident_kernel<kRuleUos, false, kQraw><<<grid, kThreads, 0, stream>>>(a); break;
+            default: attention_resident_kernel<kRuleUos, true, kQraw><<<grid, kThreads, 0, stream>>>(a); break;
         }
-        return hipGetLastError();
+        return;
     }
     switch (mode) {
-        case 0: attention_kernel<kRuleOcp, false><<<grid, kThreads, 0, stream>>>(a); break;
-        case 1: attention_kernel<kRuleUos, false><<<grid, kThreads, 0, stream>>>(a); break;
-        default: attention_kernel<kRuleUos, true><<<grid, kThreads, 0, stream>>>(a); break;
+        case 0: attention_kernel<kRuleOcp, false, kQraw><<<grid, kThreads, 0, stream>>>(a); break;
+        case 1: attention_kernel<kRuleUos, false, kQraw><<<grid, kThreads, 0, stream>>>(a); break;
+        default: attention_kernel<kRuleUos, true, kQraw><<<grid, kThreads, 0, stream>>>(a); break;
     }
+}
+
+hipError_t launch_attention(const AttnArgs& a, int mode, hipStream_t stream) {
+    const dim3 grid((unsigned)(8 * a.per_xcd));
+    if (a.qraw)
+        launch_attention_q<true>(a, mode, grid, stream);
+    else
+        launch_attention_q<false>(a, mode, grid, stream);
     return hipGetLastError();
 }
 

@@ -37,6 +37,7 @@ hipError_t launch_qmax_sse(const void* x, int axis, const double* qs, int nq, do
 struct AttnArgs {
     const uint8_t* qc;  // [BH, Nq, 64]
     const uint8_t* qs;  // [BH, Nq, 4]
+    const uint16_t* qraw;  // bf16 Q [BH, Nq, 128] if the kernel quantizes Q itself, else null
     const uint8_t* kc;  // [BH, N, 64]
     const uint8_t* ks;  // [BH, N, 4]
     const uint8_t* vc;  // [BH, 128, nb * 16]

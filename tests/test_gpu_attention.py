@@ -156,6 +156,48 @@ def test_attend_matches_forward_and_is_deterministic(mx):
         assert torch.equal(a.view(torch.int16), c.view(torch.int16))
 
 
+def _edge_q_rows(q):
+    """Overwrite the first query rows of every head with values that exercise
+    the quantizer's scale rule: an all-zero block (sigma = 1), bf16
+    subnormals, negative zeros, and block maxima exactly on and just past the
+    UOS boundary 7.25 * 2^k and the OCP boundary 2^k."""
+    q = q.copy()
+    f32 = lambda x: (np.float32(x).view(np.uint32) >> 16).astype(np.uint16)
+    for bh in range(q.shape[0] * q.shape[1]):
+        rows = q.reshape(-1, q.shape[2], q.shape[3])[bh]
+        rows[0, :32] = 0
+        rows[0, 32:64] = 0x8000  # -0
+        rows[1, :] = np.arange(1, 129, dtype=np.uint16)  # bf16 subnormals (exponent field 0)
+        rows[2, :] = f32(0.5)
+        rows[2, 0] = f32(7.25)        # UOS boundary: M = 7.25 * 2^0
+        rows[2, 32] = f32(7.28125)    # next bf16 above it
+        rows[2, 64] = f32(4.0)        # OCP boundary 2^2
+        rows[2, 96] = f32(-7.96875)   # largest bf16 below 8, negative
+    return q
+
+
+@pytest.mark.parametrize("Nkv", [300, 1000])
+def test_in_kernel_q_quantization_is_bit_exact(mx, Nkv):
+    """The forward quantizes Q inside the attention kernel (unrotated modes);
+    its output must equal the same kernel run on Q^ from the standalone
+    quantizer, bit for bit, on the resident (Nkv <= 512) and streaming paths."""
+    Nq = 300
+    wq = inputs.custom(2, 2, Nq, kind="video", index=71)
+    wk = inputs.custom(2, 2, Nkv, kind="video", index=72)
+    q = _edge_q_rows(inputs.generate(wq)[0])
+    _, k, v = inputs.generate(wk)
+    qt, kt, vt = (mx.bf16_from_bits(x) for x in (q, k, v))
+    for mode in MODES:
+        a = mx.cross_forward(qt, kt, vt, mode)
+        qc, qs = mx.quantize(qt, mx.AXIS_HEAD_DIM, mode)
+        kc, ks = mx.quantize(kt, mx.AXIS_HEAD_DIM, mode)
+        vc, vs = mx.quantize(vt, mx.AXIS_TOKENS, mode)
+        b = mx.cross_attend(qc, qs, kc, ks, vc, vs, Nq, Nkv, mode)
+        torch.cuda.synchronize()
+        log(f"[attn] in-kernel Q quantization Nkv={Nkv} mode={mode}")
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16)), (Nkv, mode)
+
+
 def test_error_paths_leave_stream_usable(mx):
     w = inputs.custom(1, 1, 64, kind="iid", index=64)
     q, k, v = inputs.generate(w)
