@@ -152,15 +152,31 @@ __global__ __launch_bounds__(256) void quantize_headdim_rot_kernel(const uint4* 
 }
 
 // ---------------------------------------------------------------------------
-// Blocks along the token axis (V).  A workgroup stages 128 tokens x 128
-// channels of one head (32 KiB of bf16) in LDS with coalesced 16-byte loads;
+// Blocks along the token axis (V).  A group of 128 tokens x 128 channels of
+// one head (32 KiB of bf16) is staged in LDS from coalesced 16-byte loads;
 // tokens past N are staged as +0 (the zero padding of the last block).  Wave w
 // then quantizes channel pairs 16w..16w+15 over the group's four 32-token
 // blocks, lane (pair p, block b) owning one block of two channels.  Output
 // rows are tokens-contiguous per channel (16 code bytes and one scale byte per
 // (channel, 32-token block)), so the four lanes of a pair write the pair's 64
-// code bytes of this group contiguously.
+// code bytes of this group contiguously.  A workgroup quantizes
+// kGroupsPerWg consecutive groups, loading the next group into registers
+// while the current one is quantized (two per workgroup measured fastest:
+// more leave too few workgroups to fill the chip evenly).
 constexpr int kVqTokens = 128;
+constexpr int kGroupsPerWg = 2;  // token groups per workgroup
+
+// Two bf16 values (a packed pair) to FP4 codes divided by `scale`, into byte
+// `sel` of `old` (the conversion takes the byte index as an immediate).
+__device__ __forceinline__ uint32_t cvt_fp4x2_bf16(uint32_t old, uint32_t pair, float scale, int sel) {
+    const bf16x2 v = __builtin_bit_cast(bf16x2, pair);
+    switch (sel) {
+        case 0: return __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(old, v, scale, 0);
+        case 1: return __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(old, v, scale, 1);
+        case 2: return __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(old, v, scale, 2);
+        default: return __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(old, v, scale, 3);
+    }
+}
 
 template <int kRule>
 __global__ __launch_bounds__(256) void quantize_tokens_kernel(const uint4* __restrict__ x,
@@ -179,75 +195,74 @@ __global__ __launch_bounds__(256) void quantize_tokens_kernel(const uint4* __res
     // reach HBM as whole lines
     const int L = blockIdx.x;
     const int logical = (L & 7) * per_xcd + (L >> 3);
-    if (logical >= total) return;
-    const int bh = logical / groups;
-    const int g = logical % groups;
-    const int tok0 = g * kVqTokens;
+    const int first = logical * kGroupsPerWg;
+    if (first >= total) return;
+    const int last = min(first + kGroupsPerWg, total);
 
-    const uint4* src = x + (int64_t)bh * N * 16;  // 16 chunks of 16 B per token
+    // group lg = (head, group) of this XCD's range, 16 chunks of 16 B per token
+    auto fetch = [&](int lg, uint4 (&r)[8]) {
+        const int bh = lg / groups, g = lg % groups;
+        const uint4* src = x + (int64_t)bh * N * 16;
 #pragma unroll
-    for (int k = 0; k < 8; k++) {
-        int ch = tid + 256 * k;  // chunk id within the group
-        int tok = ch >> 4, part = ch & 15;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (tok0 + tok < N) v = nt_load(src + (int64_t)(tok0 + tok) * 16 + part);
-        *reinterpret_cast<uint4*>(&tile[tok * 64 + ((part * 4) ^ (16 * (tok >> 5)))]) = v;
-    }
-    __syncthreads();
-
-    // wave w: channel pairs 16 w .. 16 w + 15; lane: pair p = lane / 4, token
-    // block b = lane % 4 of the group.  The four lanes of a pair write the
-    // pair's four 16-byte code chunks of this group next to each other.
-    const int w = tid >> 6, lane = tid & 63;
-    const int p = lane >> 2, b = lane & 3;
-    const int cp = 16 * w + p;  // channels 2cp, 2cp+1 (dword column cp)
-    const int blk = 4 * g + b;
-    if (blk >= nb) return;
-
-    uint32_t col[32];
-    uint32_t m0 = 0, m1 = 0;
+        for (int k = 0; k < 8; k++) {
+            const int ch = tid + 256 * k;
+            const int tok = ch >> 4, part = ch & 15;
+            r[k] = (g * kVqTokens + tok < N) ? nt_load(src + (int64_t)(g * kVqTokens + tok) * 16 + part)
+                                             : make_uint4(0, 0, 0, 0);
+        }
+    };
+    uint4 buf[8];
+    fetch(first, buf);
+    for (int lg = first; lg < last; lg++) {
+        __syncthreads();  // the previous group's LDS reads are done
 #pragma unroll
-    for (int t = 0; t < 32; t++) {
-        uint32_t d = tile[(32 * b + t) * 64 + (cp ^ (16 * b))];
-        col[t] = d;
-        m0 = max(m0, d & 0x7FFFu);
-        m1 = max(m1, (d >> 16) & 0x7FFFu);
-    }
-    const uint32_t s0 = (m0 == 0) ? 127u : (uint32_t)(block_exponent_bf16<kRule>(m0, bq) + 127);
-    const uint32_t s1 = (m1 == 0) ? 127u : (uint32_t)(block_exponent_bf16<kRule>(m1, bq) + 127);
-    const float f0 = e8m0_as_f32(s0), f1 = e8m0_as_f32(s1);
+        for (int k = 0; k < 8; k++) {
+            const int ch = tid + 256 * k;
+            const int tok = ch >> 4, part = ch & 15;
+            *reinterpret_cast<uint4*>(&tile[tok * 64 + ((part * 4) ^ (16 * (tok >> 5)))]) = buf[k];
+        }
+        __syncthreads();
+        if (lg + 1 < last) fetch(lg + 1, buf);  // in flight while this group is quantized
+        const int bh = lg / groups, g = lg % groups;
 
-    uint32_t c0[4] = {0, 0, 0, 0}, c1[4] = {0, 0, 0, 0};
+        // wave w: channel pairs 16 w .. 16 w + 15; lane: pair p = lane / 4, token
+        // block b = lane % 4 of the group.  The four lanes of a pair write the
+        // pair's four 16-byte code chunks of this group next to each other.
+        const int w = tid >> 6, lane = tid & 63;
+        const int p = lane >> 2, b = lane & 3;
+        const int cp = 16 * w + p;  // channels 2cp, 2cp+1 (dword column cp)
+        const int blk = 4 * g + b;
+        if (blk < nb) {
+            uint32_t col[32];
+            uint32_t m0 = 0, m1 = 0;
 #pragma unroll
-    for (int t = 0; t < 32; t += 2) {
-        // (token t, token t+1) pairs of each channel
-        uint32_t lo = __builtin_amdgcn_perm(col[t + 1], col[t], 0x05040100u);  // low halves
-        uint32_t hi = __builtin_amdgcn_perm(col[t + 1], col[t], 0x07060302u);  // high halves
-        const int word = t >> 3, sel = (t & 7) >> 1;
-        switch (sel) {
-            case 0:
-                c0[word] = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c0[word], __builtin_bit_cast(bf16x2, lo), f0, 0);
-                c1[word] = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c1[word], __builtin_bit_cast(bf16x2, hi), f1, 0);
-                break;
-            case 1:
-                c0[word] = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c0[word], __builtin_bit_cast(bf16x2, lo), f0, 1);
-                c1[word] = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c1[word], __builtin_bit_cast(bf16x2, hi), f1, 1);
-                break;
-            case 2:
-                c0[word] = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c0[word], __builtin_bit_cast(bf16x2, lo), f0, 2);
-                c1[word] = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c1[word], __builtin_bit_cast(bf16x2, hi), f1, 2);
-                break;
-            default:
-                c0[word] = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c0[word], __builtin_bit_cast(bf16x2, lo), f0, 3);
-                c1[word] = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(c1[word], __builtin_bit_cast(bf16x2, hi), f1, 3);
-                break;
+            for (int t = 0; t < 32; t++) {
+                uint32_t d = tile[(32 * b + t) * 64 + (cp ^ (16 * b))];
+                col[t] = d;
+                m0 = max(m0, d & 0x7FFFu);
+                m1 = max(m1, (d >> 16) & 0x7FFFu);
+            }
+            const uint32_t s0 = (m0 == 0) ? 127u : (uint32_t)(block_exponent_bf16<kRule>(m0, bq) + 127);
+            const uint32_t s1 = (m1 == 0) ? 127u : (uint32_t)(block_exponent_bf16<kRule>(m1, bq) + 127);
+            const float f0 = e8m0_as_f32(s0), f1 = e8m0_as_f32(s1);
+
+            uint32_t c0[4] = {0, 0, 0, 0}, c1[4] = {0, 0, 0, 0};
+#pragma unroll
+            for (int t = 0; t < 32; t += 2) {
+                // (token t, token t+1) pairs of each channel
+                uint32_t lo = __builtin_amdgcn_perm(col[t + 1], col[t], 0x05040100u);  // low halves
+                uint32_t hi = __builtin_amdgcn_perm(col[t + 1], col[t], 0x07060302u);  // high halves
+                const int word = t >> 3, sel = (t & 7) >> 1;
+                c0[word] = cvt_fp4x2_bf16(c0[word], lo, f0, sel);
+                c1[word] = cvt_fp4x2_bf16(c1[word], hi, f1, sel);
+            }
+            const int64_t row0 = (int64_t)bh * 128 + 2 * cp;
+            *reinterpret_cast<uint4*>(codes + (row0 * nb + blk) * 16) = make_uint4(c0[0], c0[1], c0[2], c0[3]);
+            *reinterpret_cast<uint4*>(codes + ((row0 + 1) * nb + blk) * 16) = make_uint4(c1[0], c1[1], c1[2], c1[3]);
+            scales[row0 * nb + blk] = (uint8_t)s0;
+            scales[(row0 + 1) * nb + blk] = (uint8_t)s1;
         }
     }
-    const int64_t row0 = (int64_t)bh * 128 + 2 * cp;
-    *reinterpret_cast<uint4*>(codes + (row0 * nb + blk) * 16) = make_uint4(c0[0], c0[1], c0[2], c0[3]);
-    *reinterpret_cast<uint4*>(codes + ((row0 + 1) * nb + blk) * 16) = make_uint4(c1[0], c1[1], c1[2], c1[3]);
-    scales[row0 * nb + blk] = (uint8_t)s0;
-    scales[(row0 + 1) * nb + blk] = (uint8_t)s1;
 }
 
 // Kernel argument of the kRuleQmax rule for boundary q (4 <= q <= 8).
@@ -295,7 +310,8 @@ hipError_t launch_quantize_tokens(const void* x, uint8_t* codes, uint8_t* scales
     const int nb = (int)((N + 31) / 32);
     const int groups = (int)((N + kVqTokens - 1) / kVqTokens);
     const int total = (int)(BH * groups);
-    const int per_xcd = (total + 7) / 8;
+    const int wgs = (total + kGroupsPerWg - 1) / kGroupsPerWg;
+    const int per_xcd = (wgs + 7) / 8;
     const dim3 grid((unsigned)(8 * per_xcd));
     const Boundary bq = boundary_of(rule == kRuleQmax ? qmax : 7.25);
     if (rule == kRuleUos)
