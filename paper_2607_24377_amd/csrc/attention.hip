@@ -66,6 +66,12 @@ constexpr int kVcOff = 8192;   // V^ codes: 128 rows (channels) x 64 B (128 keys
 constexpr int kKsOff = 16384;  // K^ scales: 64 lanes x 8 B, in MFMA operand order
 constexpr int kVsOff = 16896;  // V^ scales: 64 lanes x 8 B, in MFMA operand order
 constexpr int kStageBytes = 17408;
+constexpr int kOutStageBytes = 2048;  // per wave: 8 output rows of 256 B
+// Short key sequences are bound by the output stores, long ones by the
+// softmax: the resident kernel stages its output rows through LDS (fully
+// coalesced 1 KiB stores, four dependent LDS round trips) up to this many
+// key tiles and stores 16 bytes per lane directly above it.
+constexpr int kStagedStoreMaxTiles = 2;
 
 // 16-byte slot swizzle of a 64-byte LDS row: any 16 consecutive rows read at
 // the same logical slot hit 16 distinct 16-byte bank groups.
@@ -520,8 +526,9 @@ __device__ __forceinline__ void attend_tile(const LdsLane& la, int tile, int N, 
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 template <bool kPnq>
-__device__ __forceinline__ void store_rows(const AttnArgs& a, int64_t rowbase, int qi, int q, int h,
-                                           const RowSum& rs, const v16f (&O)[4]) {
+__device__ __forceinline__ void store_rows(const AttnArgs& a, int64_t rowbase, int qi, int q, int h, int lane,
+                                           uint8_t* stage, bool staged, const RowSum& rs,
+                                           const v16f (&O)[4]) {
     float ltot;
     if (kPnq) {
         // the sums of queries q and q + 16 sit in lane q & 15 (RowSum)
@@ -531,20 +538,74 @@ __device__ __forceinline__ void store_rows(const AttnArgs& a, int64_t rowbase, i
         ltot = rs.l + __shfl_xor(rs.l, 32);
     }
     const float inv = 1.0f / ltot;  // one division, then 64 products
-    if (qi < a.Nq) {
-        uint16_t* orow = a.out + (int64_t)(rowbase + qi) * 128;
+    // w[n][g]: channels 32 n + 8 g + 4 h .. + 3 of the row as two bf16 pairs
+    // (round to nearest even with the packed hardware conversion)
+    uint32_t w[4][4][2];
 #pragma unroll
-        for (int n = 0; n < 4; n++) {
+    for (int n = 0; n < 4; n++)
 #pragma unroll
-            for (int g = 0; g < 4; g++) {
-                // round to nearest even with the packed hardware conversion
-                const f32x2 lo = {O[n][4 * g + 0] * inv, O[n][4 * g + 1] * inv};
-                const f32x2 hi = {O[n][4 * g + 2] * inv, O[n][4 * g + 3] * inv};
-                *reinterpret_cast<uint2*>(orow + 32 * n + 8 * g + 4 * h) =
-                    make_uint2(__builtin_bit_cast(uint32_t, __builtin_convertvector(lo, bf16x2)),
-                               __builtin_bit_cast(uint32_t, __builtin_convertvector(hi, bf16x2)));
-            }
+        for (int g = 0; g < 4; g++) {
+            const f32x2 lo = {O[n][4 * g + 0] * inv, O[n][4 * g + 1] * inv};
+            const f32x2 hi = {O[n][4 * g + 2] * inv, O[n][4 * g + 3] * inv};
+            w[n][g][0] = __builtin_bit_cast(uint32_t, __builtin_convertvector(lo, bf16x2));
+            w[n][g][1] = __builtin_bit_cast(uint32_t, __builtin_convertvector(hi, bf16x2));
         }
+    // Lanes q and q + 32 hold the row's channel groups 8 g .. 8 g + 7 in
+    // halves.  Swapping the lanes 32-63 of the even-g words with the lanes
+    // 0-31 of the odd-g words gives lane h all eight channels of group
+    // g = 2 j + h, i.e. 16 contiguous bytes per (n, j).
+#pragma unroll
+    for (int n = 0; n < 4; n++)
+#pragma unroll
+        for (int j = 0; j < 2; j++)
+#pragma unroll
+            for (int k = 0; k < 2; k++) {
+                const auto r = __builtin_amdgcn_permlane32_swap(w[n][2 * j][k], w[n][2 * j + 1][k], false, false);
+                w[n][2 * j][k] = (uint32_t)r[0];
+                w[n][2 * j + 1][k] = (uint32_t)r[1];
+            }
+    if (!staged) {
+        if (qi < a.Nq) {
+            uint16_t* dst = a.out + (rowbase + qi) * 128 + 8 * h;
+#pragma unroll
+            for (int n = 0; n < 4; n++)
+#pragma unroll
+                for (int j = 0; j < 2; j++)
+                    *reinterpret_cast<uint4*>(dst + 32 * n + 16 * j) =
+                        make_uint4(w[n][2 * j][0], w[n][2 * j][1], w[n][2 * j + 1][0], w[n][2 * j + 1][1]);
+        }
+        return;
+    }
+    // Staged: the wave's 32 output rows are contiguous in memory (8 KiB).
+    // They go through the wave's 2 KiB LDS buffer 8 rows at a time: the 16
+    // lanes of those rows write them in, then every lane copies 2 x 16 bytes
+    // out, so each store instruction writes 1 KiB of consecutive rows.  The
+    // 16-byte slot of a row is XOR-ed with the row index to spread the writes
+    // of the 8 rows over the banks.
+    const int q0 = qi - q;  // first row of the wave
+#pragma unroll
+    for (int pass = 0; pass < 4; pass++) {
+        if ((q >> 3) == pass) {
+            const int row = q & 7;
+#pragma unroll
+            for (int n = 0; n < 4; n++)
+#pragma unroll
+                for (int j = 0; j < 2; j++) {
+                    const int slot = (4 * n + 2 * j + h) ^ row;
+                    *reinterpret_cast<uint4*>(stage + row * 256 + slot * 16) =
+                        make_uint4(w[n][2 * j][0], w[n][2 * j][1], w[n][2 * j + 1][0], w[n][2 * j + 1][1]);
+                }
+        }
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int k = 0; k < 2; k++) {
+            const int byte = 1024 * k + 16 * lane;  // of the 8 rows, 2 KiB
+            const int row = byte >> 8, slot = (byte >> 4) & 15;
+            const uint4 v = *reinterpret_cast<const uint4*>(stage + row * 256 + (slot ^ row) * 16);
+            const int r = q0 + 8 * pass + row;
+            if (r < a.Nq) *reinterpret_cast<uint4*>(a.out + (int64_t)(rowbase + r) * 128 + slot * 8) = v;
+        }
+        __builtin_amdgcn_wave_barrier();
     }
 }
 
@@ -613,7 +674,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
         if (tile + 2 >= ntiles) break;
     }
 
-    store_rows<kPnq>(a, rowbase, qi, q, h, rs, O);
+    store_rows<kPnq>(a, rowbase, qi, q, h, lane, nullptr, false, rs, O);
 }
 
 // Short key sequences (cross-attention over a text context, at most
@@ -622,6 +683,8 @@ __global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
 // with no per-tile loads or barriers; each query tile is the same computation
 // as in attention_kernel.
 constexpr int kResidentTiles = kResidentKeys / 128;
+static_assert(kStagedStoreMaxTiles < kResidentTiles && kWaves * kOutStageBytes <= kStageBytes,
+              "the output staging buffers fit in an unused tile slot");
 
 template <int kRule, bool kPnq, bool kQraw>
 __global__ __launch_bounds__(kThreads, 2) void attention_resident_kernel(AttnArgs a) {
@@ -642,6 +705,9 @@ __global__ __launch_bounds__(kThreads, 2) void attention_resident_kernel(AttnArg
     const int Nq = a.Nq;
     const int64_t rowbase = (int64_t)bh * Nq;
     const int ntiles = (N + 127) / 128;
+    // staging goes to the first unused tile slot
+    const bool staged = ntiles <= kStagedStoreMaxTiles;
+    uint8_t* const ostage = lds + ntiles * kStageBytes + wave * kOutStageBytes;
 
     const TileLoader loader(a, bh, wave, lane);
     for (int t = 0; t < ntiles; t++) loader.load(lds + t * kStageBytes, t);
@@ -661,15 +727,16 @@ __global__ __launch_bounds__(kThreads, 2) void attention_resident_kernel(AttnArg
         else
             return q_operands(a, q_row(qt), h);
     };
+    // Quantized operands are taken over at the top of the loop; raw rows are
+    // quantized before the epilogue instead, so that their 32 registers are
+    // not held through it (each order measured faster for its own kind).
     QFetch next = fetch(qt0);
+    QOperands qo;
+    if constexpr (kQraw) qo = quantize_q<kRule>(next);
 
     for (int qt = qt0; qt < qt1; qt++) {
         const int qi = qt * kQueryTile + wave * kQw + q;
-        QOperands qo;
-        if constexpr (kQraw)
-            qo = quantize_q<kRule>(next);
-        else
-            qo = next;
+        if constexpr (!kQraw) qo = next;
         if (qt + 1 < qt1) next = fetch(qt + 1);
 
         float m = -__builtin_inff();
@@ -686,7 +753,9 @@ __global__ __launch_bounds__(kThreads, 2) void attention_resident_kernel(AttnArg
             attend_tile<kRule, kPnq, 0>(lds_lane(lds + tile * kStageBytes, q, h, lane), tile, N, h, qo, sel, m,
                                         rs, O);
 
-        store_rows<kPnq>(a, rowbase, qi, q, h, rs, O);
+        if constexpr (kQraw)
+            if (qt + 1 < qt1) qo = quantize_q<kRule>(next);
+        store_rows<kPnq>(a, rowbase, qi, q, h, lane, ostage, staged, rs, O);
     }
 }
 
