@@ -366,7 +366,10 @@ __device__ __forceinline__ QOperands quantize_q(const QRaw& r) {
 // One KV tile of Algorithm 2 for the wave's 32 query rows, on LDS stage
 // kStage (relative to la): S^T = K^ Q^T, the online-softmax update of (m, l),
 // P^ and O~^T += V^T P^T.  Reads LDS only; the caller owns loads and barriers.
-template <int kRule, bool kPnq, int kStage>
+// kFirst: the row's first tile, which sets m, l and O~ instead of updating
+// them (the rescale by alpha = 0 of a zero O~ and l is skipped, and the first
+// products accumulate onto zero), so they need no initial values.
+template <int kRule, bool kPnq, int kStage, bool kFirst = false>
 __device__ __forceinline__ void attend_tile(const LdsLane& la, int tile, int N, int h,
                                             const QOperands& qo, const v8i& sel, float& m, RowSum& rs,
                                             v16f (&O)[4]) {
@@ -454,8 +457,8 @@ __device__ __forceinline__ void attend_tile(const LdsLane& la, int tile, int N, 
 #pragma unroll
     for (int c = 0; c < 2; c++) bmax[c] = block_max32(S[c][0], S[c][1]);
     float rmax = max_with_other_half(max2f(bmax[0], bmax[1]));
-    const float m_new = max2f(m, mul_rd(cl, rmax));
-    const float alpha = __builtin_amdgcn_exp2f(m - m_new);  // 0 on the first tile
+    const float m_new = kFirst ? mul_rd(cl, rmax) : max2f(m, mul_rd(cl, rmax));
+    const float alpha = kFirst ? 0.f : __builtin_amdgcn_exp2f(m - m_new);  // 0 on the first tile
     m = m_new;
 
     // ---- O~^T rescale and V^ operands, then per 64-key chunk: P~ -> P^ and
@@ -470,7 +473,7 @@ __device__ __forceinline__ void attend_tile(const LdsLane& la, int tile, int N, 
         vop[n][0] = fp4_v(vr[n][0]);
         vop[n][1] = fp4_v(vr[n][1]);
     }
-    if (__any(alpha != 1.f)) {
+    if (!kFirst && __any(alpha != 1.f)) {
 #pragma unroll
         for (int n = 0; n < 4; n++)
 #pragma unroll
@@ -503,6 +506,15 @@ __device__ __forceinline__ void attend_tile(const LdsLane& la, int tile, int N, 
             w[n >> 3] = cvt_fp4x2(prev, p0, p1, sf, (n & 7) >> 1);
         }
         const v8i P = fp4_operand(make_uint4(w[0], w[1], w[2], w[3]));
+        if (kFirst && c == 0) {
+            const v16f zero = {};
+            if (kPnq) rs.L = mfma16_fp4(sel, P, v4f{0.f, 0.f, 0.f, 0.f}, 127, psc);
+            O[0] = mfma_fp4<0>(vop[0][0], P, zero, (int)vsb.x, psc);
+            O[1] = mfma_fp4<2>(vop[1][0], P, zero, (int)vsb.x, psc);
+            O[2] = mfma_fp4<0>(vop[2][0], P, zero, (int)vsb.y, psc);
+            O[3] = mfma_fp4<2>(vop[3][0], P, zero, (int)vsb.y, psc);
+            continue;
+        }
         if (kPnq) rs.L = mfma16_fp4(sel, P, rs.L, 127, psc);
         // scale byte 2 (n & 1) + c of the register of channel rows 32 n
         if (c == 0) {
@@ -517,7 +529,7 @@ __device__ __forceinline__ void attend_tile(const LdsLane& la, int tile, int N, 
             O[3] = mfma_fp4<3>(vop[3][1], P, O[3], (int)vsb.y, psc);
         }
     }
-    if (!kPnq) rs.l = alpha * rs.l + lsum;
+    if (!kPnq) rs.l = kFirst ? lsum : alpha * rs.l + lsum;
 }
 
 // O = O~ / l rounded to bf16 (Eq. online_attention_output), as O~ times the
@@ -739,17 +751,12 @@ __global__ __launch_bounds__(kThreads, 2) void attention_resident_kernel(AttnArg
         if constexpr (!kQraw) qo = next;
         if (qt + 1 < qt1) next = fetch(qt + 1);
 
-        float m = -__builtin_inff();
+        // set by the first tile (N >= 1, so there is one)
+        float m;
         RowSum rs;
-        rs.l = 0.f;
-        rs.L = v4f{0.f, 0.f, 0.f, 0.f};
         v16f O[4];
-#pragma unroll
-        for (int n = 0; n < 4; n++)
-#pragma unroll
-            for (int i = 0; i < 16; i++) O[n][i] = 0.f;
-
-        for (int tile = 0; tile < ntiles; tile++)
+        attend_tile<kRule, kPnq, 0, true>(lds_lane(lds, q, h, lane), 0, N, h, qo, sel, m, rs, O);
+        for (int tile = 1; tile < ntiles; tile++)
             attend_tile<kRule, kPnq, 0>(lds_lane(lds + tile * kStageBytes, q, h, lane), tile, N, h, qo, sel, m,
                                         rs, O);
 
