@@ -26,7 +26,7 @@ if ROOT not in sys.path:
 METRIC = "MXFP4 attn fwd TFLOPS (4·B·H·N²·d/t) & % of MXFP4 MFMA peak, N=75600"
 PEAK_FP4_TFLOPS = 10100.0  # MI355X dense MXFP4 matrix-core peak, 10.1 PFLOP/s
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 matrix-core peak, 2.5 PFLOP/s
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attention_video720p_hbm_traffic.json")
+PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_24377_amd", "csrc", "attention.hip")
 
 
@@ -50,15 +50,17 @@ def time_ms(fn, steps: int, warmup: int, torch) -> float:
     return start.elapsed_time(end) / steps
 
 
-def measured_traffic():
+def measured_traffic(workload: str, mode: str):
     """HBM bytes per launch of the attention kernel from the committed PMC
-    counter summary, if it was taken on the current kernel source."""
+    counter summary of this workload and mode, if it was taken on the current
+    kernel source."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(os.path.join(PROFILES, f"attention_{workload}_hbm_traffic.json")) as f:
             rec = json.load(f)
         with open(KERNEL_SOURCE, "rb") as f:
             sha = hashlib.sha256(f.read()).hexdigest()
-        if rec.get("kernel_source_sha256") != sha:
+        if (rec.get("kernel_source_sha256") != sha or rec.get("workload_name") != workload
+                or rec.get("mode") != mode):
             return None
         return float(rec["hbm_bytes_per_launch"])
     except (OSError, ValueError, KeyError):
@@ -250,7 +252,7 @@ def main():
                    "kv_tile": mxattn.kv_tile(), "query_tile": mxattn.query_tile()},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP4_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_FP4_TFLOPS,
-                     "traffic": measured_traffic()},
+                     "traffic": measured_traffic(w.name, args.mode)},
     }
     result.update(extra)
     if not args.no_cpu_baseline:
