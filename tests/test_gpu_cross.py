@@ -63,8 +63,8 @@ def test_cross_ragged_all_rows(mx, mode):
 
 
 @pytest.mark.parametrize("Nq,Nkv", [(200, 1), (200, 31), (1, 200), (129, 32), (130, 33), (300, 128),
-                                    (64, 129), (257, 255), (300, 512), (300, 513), (130, 640),
-                                    (64, 1100)])
+                                    (64, 129), (257, 255), (130, 257), (200, 384), (300, 512),
+                                    (300, 513), (130, 640), (64, 1100)])
 def test_cross_ragged_lengths(mx, Nq, Nkv):
     w = inputs.Workload(60 + Nkv % 5, f"cross_{Nq}x{Nkv}", 2, 2, Nq, 128, "cross", Nkv=Nkv)
     for mode in ("ocp_vanilla", "uos_pnq"):
@@ -90,4 +90,14 @@ def test_resident_several_query_tiles_per_workgroup(mx):
     w = inputs.Workload(71, "cross_16x16500x500", 1, 16, 16500, 128, "cross", Nkv=500)
     for mode in ("ocp_vanilla", "uos_pnq"):
         _check(mx, w, mode, [0, 7, 15], 40, w.name)
+    torch.cuda.empty_cache()
+
+
+def test_resident_staged_stores_several_query_tiles(mx):
+    # up to two key tiles the output rows go through an LDS buffer that each
+    # query tile of a workgroup reuses: 16 heads x 129 query tiles, two per
+    # workgroup, 200 keys (a full and a partial tile)
+    w = inputs.Workload(72, "cross_16x16500x200", 1, 16, 16500, 128, "cross", Nkv=200)
+    for mode in ("ocp_vanilla", "uos_pnq"):
+        _check(mx, w, mode, [0, 9, 15], 40, w.name)
     torch.cuda.empty_cache()
