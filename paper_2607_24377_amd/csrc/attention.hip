@@ -739,17 +739,27 @@ __global__ __launch_bounds__(kThreads, 2) void attention_resident_kernel(AttnArg
         else
             return q_operands(a, q_row(qt), h);
     };
-    // Quantized operands are taken over at the top of the loop; raw rows are
-    // quantized before the epilogue instead, so that their 32 registers are
-    // not held through it (each order measured faster for its own kind).
-    QFetch next = fetch(qt0);
-    QOperands qo;
-    if constexpr (kQraw) qo = quantize_q<kRule>(next);
+    // The next query tile's operands are formed from its fetched rows before
+    // this tile's output stores are issued.  vmcnt counts loads and stores
+    // alike and the number of stores is not static (row guards, staging), so a
+    // wait for the fetched registers placed after the stores would wait for
+    // the stores as well, once per query tile.  Quantized operands are read
+    // by an empty asm statement to pin that wait before the stores; raw rows
+    // are read by their quantization.
+    auto operands = [&](QFetch f) -> QOperands {
+        if constexpr (kQraw) {
+            return quantize_q<kRule>(f);
+        } else {
+            asm volatile("" : "+v"(f.b0), "+v"(f.b1), "+v"(f.s0), "+v"(f.s1));
+            return f;
+        }
+    };
+    QOperands qo = operands(fetch(qt0));
 
     for (int qt = qt0; qt < qt1; qt++) {
         const int qi = qt * kQueryTile + wave * kQw + q;
-        if constexpr (!kQraw) qo = next;
-        if (qt + 1 < qt1) next = fetch(qt + 1);
+        // the last query tile fetches itself again: no branch around the loads
+        const QFetch next = fetch(min(qt + 1, qt1 - 1));
 
         // set by the first tile (N >= 1, so there is one)
         float m;
@@ -760,9 +770,9 @@ __global__ __launch_bounds__(kThreads, 2) void attention_resident_kernel(AttnArg
             attend_tile<kRule, kPnq, 0>(lds_lane(lds + tile * kStageBytes, q, h, lane), tile, N, h, qo, sel, m,
                                         rs, O);
 
-        if constexpr (kQraw)
-            if (qt + 1 < qt1) qo = quantize_q<kRule>(next);
+        const QOperands qn = operands(next);
         store_rows<kPnq>(a, rowbase, qi, q, h, lane, ostage, staged, rs, O);
+        qo = qn;
     }
 }
 
