@@ -280,8 +280,10 @@ def attention_rows(q: np.ndarray, k: np.ndarray, v: np.ndarray, p_rule: int, pnq
     """Tiled online-softmax attention of the given query rows against one head.
 
     q [R, d], k [N, d], v [N, d] (doubles).  Returns O [R, d] in fp64 and, if
-    ``diag``, a [R, 6] array (l, induced row sum, unrolled l, max |O - O_unrolled|,
-    tiles, max rises)."""
+    ``diag``, a [R, 8] array (l, induced row sum, unrolled l, max |O - O_unrolled|,
+    tiles, max rises, P~ elements within 4 fp32 ulps of an E2M1 decision
+    threshold, blocks whose maximum is within 4 fp32 ulps of an end of the
+    scale rule's range)."""
     q = np.ascontiguousarray(q, dtype=np.float64)
     k = np.ascontiguousarray(k, dtype=np.float64)
     v = np.ascontiguousarray(v, dtype=np.float64)
@@ -289,7 +291,7 @@ def attention_rows(q: np.ndarray, k: np.ndarray, v: np.ndarray, p_rule: int, pnq
     N = k.shape[0]
     assert k.shape == (N, d) and v.shape == (N, d)
     out = np.empty((R, d), dtype=np.float64)
-    dg = np.empty((R, 6), dtype=np.float64) if diag else None
+    dg = np.empty((R, 8), dtype=np.float64) if diag else None
     rc = lib().mxref_attention_rows(_ptr(q), _ptr(k), _ptr(v), N, d, R, p_rule, pnq, exact,
                                     block_c, _ptr(out), _ptr(dg) if diag else None, nthreads)
     if rc != 0:

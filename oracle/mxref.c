@@ -515,11 +515,57 @@ void mxref_dequant_keys(const uint8_t* codes, const uint8_t* scales, int64_t N, 
  *   exact  0: kernel fp32 contract for s, m', t, p~; 1: fp64 throughout
  *   block_c KV tile width (a multiple of 32 unless p_rule is identity)
  *   out    [n_rows, d] O = O~ / l in fp64
- *   diag   [n_rows, 6] or NULL:
+ *   diag   [n_rows, 8] or NULL:
  *          0 l, 1 induced row sum (sum_j beta_j sum P^_j) / l,
  *          2 l rebuilt from the unrolled form, 3 max |O - O_unrolled|,
- *          4 number of tiles, 5 number of tiles where the max rose
+ *          4 number of tiles, 5 number of tiles where the max rose,
+ *          6 elements of P~ within 4 fp32 ulps of an E2M1 decision threshold
+ *            of their block (near_threshold), 7 blocks whose maximum lies
+ *            within 4 fp32 ulps of an end of its scale rule's range
+ *            (near_boundary).  Columns 6 and 7 audit the exponential: an
+ *            exp2 that is faithful rather than correctly rounded can move
+ *            exactly these elements to a neighbouring code (or these blocks
+ *            to a neighbouring scale); every other element's code is fixed
+ *            by the fp32 argument t alone.
  */
+/* Distance, in units of the fp32 spacing just above x > 0, within which a
+ * value counts as "near" a decision point in the exponential audit. */
+static int near_f32(double x, double point) {
+    const float xf = (float)x;
+    const double ulp = (double)nextafterf(xf, INFINITY) - (double)xf;
+    return fabs(x - point) <= 4.0 * ulp;
+}
+
+/* E2M1 decision thresholds: the midpoints between neighbouring grid values
+ * (App. B), in units of the block scale. */
+static const double E2M1_MIDPOINTS[7] = {0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0};
+
+/* Audit of one quantized block of fp32 exponentials p[0..n) with scale byte
+ * sc: adds the number of elements near a decision threshold to *near_el and
+ * one to *near_blk when the block maximum is near an end of the rule's
+ * normalized range (UOS (3.625, 7.25] sigma, OCP [4, 8) sigma), unless the
+ * block holds the row maximum. */
+static void audit_block(const double* p, int64_t n, uint8_t sc, int rule, double* near_el,
+                        double* near_blk) {
+    const double sigma = ldexp(1.0, (int)sc - 127);
+    double M = 0.0;
+    for (int64_t i = 0; i < n; i++) {
+        if (p[i] > M) M = p[i];
+        if (!(p[i] > 0.0)) continue;
+        for (int k = 0; k < 7; k++)
+            if (near_f32(p[i], E2M1_MIDPOINTS[k] * sigma)) {
+                *near_el += 1.0;
+                break;
+            }
+    }
+    /* a block holding the row maximum has M in [1, 1 + 2^-20]: exp2 of an
+     * argument t >= 0 is never below 1, so its scale cannot move */
+    if (!(M > 0.0) || M >= 1.0) return;
+    const double lo = (rule == RULE_UOS ? 0.5 * UOS_QMAX : 4.0) * sigma;
+    const double hi = (rule == RULE_UOS ? UOS_QMAX : 8.0) * sigma;
+    if (near_f32(M, lo) || near_f32(M, hi)) *near_blk += 1.0;
+}
+
 typedef struct {
     const double* q;
     const double* k;
@@ -556,6 +602,7 @@ static void attn_range(void* p, int64_t r0, int64_t r1) {
     for (int64_t r = r0; r < r1; r++) {
         const double* qr = A->q + r * d;
         double m = -INFINITY, l = 0.0;
+        double near_el = 0.0, near_blk = 0.0;
         int rises = 0;
         for (int64_t c = 0; c < d; c++) o[c] = 0.0;
 
@@ -610,6 +657,7 @@ static void attn_range(void* p, int64_t r0, int64_t r1) {
                     if (nv > 32) nv = 32;
                     uint8_t sc = quantize_block(pt + b, 32, A->p_rule, cd);
                     for (int64_t t = 0; t < nv; t++) ph[b + t] = mxref_decode(cd[t], sc);
+                    if (A->diag && !A->exact) audit_block(pt + b, nv, sc, A->p_rule, &near_el, &near_blk);
                 }
             }
 
@@ -658,13 +706,15 @@ static void attn_range(void* p, int64_t r0, int64_t r1) {
                 double df = fabs(ou / lu - orow[c]);
                 if (df > maxdiff) maxdiff = df;
             }
-            double* dg = A->diag + r * 6;
+            double* dg = A->diag + r * 8;
             dg[0] = l;
             dg[1] = mass / l;
             dg[2] = lu;
             dg[3] = maxdiff;
             dg[4] = (double)ntiles;
             dg[5] = (double)rises;
+            dg[6] = near_el;
+            dg[7] = near_blk;
         }
     }
     free(s);

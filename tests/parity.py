@@ -67,3 +67,93 @@ def oracle_rows(codes: dict, head: int, N: int, rows, mode: str, block_c: int, d
 def flat(a: np.ndarray) -> np.ndarray:
     """[B, H, ...] -> [B*H, ...]."""
     return a.reshape((-1,) + a.shape[2:])
+
+
+# Full-size parity sample: at least this many query rows per workload, spread
+# evenly over every (batch, head).
+FULL_SAMPLE_ROWS = 2048
+
+
+def stratified_rows(N: int, head: int, n_heads: int, per_head: int, seed: int, text_tokens: int = 0,
+                    tile: int = 128):
+    """Query rows of one head for the full-size parity sample: rows of the
+    first query tile (0, 1, 63, 127), of the ragged last query tile (its first
+    two rows and the last two of the sequence), this head's share of the text
+    rows (every n_heads-th one, so that the heads together cover each text row
+    exactly once), and random rows up to per_head."""
+    rng = np.random.default_rng(seed)
+    rows = {r for r in (0, 1, 63, 127) if r < N}
+    last = (N - 1) // tile * tile
+    rows |= {r for r in (last, last + 1, N - 2, N - 1) if 0 <= r < N}
+    if text_tokens:
+        rows |= set(range(N - text_tokens + head % n_heads, N, n_heads))
+    while len(rows) < min(per_head, N):
+        rows.add(int(rng.integers(N)))
+    return np.array(sorted(rows), dtype=np.int64)
+
+
+def gpu_codes(mx, qt, kt, vt, mode):
+    """The GPU quantizer's codes and scales of Q, K, V as host arrays [BH, ...]."""
+    qc, qs = mx.quantize(qt, mx.AXIS_HEAD_DIM, mode)
+    kc, ks = mx.quantize(kt, mx.AXIS_HEAD_DIM, mode)
+    vc, vs = mx.quantize(vt, mx.AXIS_TOKENS, mode)
+    return {n: flat(t.cpu().numpy()) for n, t in dict(qc=qc, qs=qs, kc=kc, ks=ks, vc=vc, vs=vs).items()}
+
+
+@functools.lru_cache(maxsize=8)
+def full_size_rows(cfg: int):
+    """{head: rows} of the full-size sample of workload `cfg` (mode-independent)."""
+    w = inputs.workload(cfg)
+    BH = w.B * w.H
+    per_head = -(-FULL_SAMPLE_ROWS // BH)
+    return {h: stratified_rows(w.N, h, BH, per_head, 5000 * cfg + h, w.text_tokens) for h in range(BH)}
+
+
+@functools.lru_cache(maxsize=8)
+def exact_reference(cfg: int):
+    """Exact fp64 attention (no quantization) of the full-size sample's rows,
+    in the same order as full_size_sample's arrays."""
+    w = inputs.workload(cfg)
+    q, k, v = (flat(x) for x in workload_bits(cfg))
+    out = []
+    for h, rows in full_size_rows(cfg).items():
+        out.append(oracle.attention_exact_rows(oracle.bf16_to_f64(q[h][rows]), oracle.bf16_to_f64(k[h]),
+                                               oracle.bf16_to_f64(v[h])))
+    return np.concatenate(out)
+
+
+@functools.lru_cache(maxsize=32)
+def full_size_sample(cfg: int, mode: str):
+    """The forward of workload `cfg` on the GPU (the launch the benchmark
+    times) and the oracle, fed the GPU's own codes, on >= FULL_SAMPLE_ROWS
+    stratified rows covering every head.  Cached so that the parity test
+    and the error report share one sample.
+
+    Returns dict(rows={head: rows}, got, ref, ref64 [R, d] in head order,
+    diag [R, 8] (oracle diagnostics), head_of [R])."""
+    import torch
+
+    from paper_2607_24377_amd import mxattn as mx
+
+    w = inputs.workload(cfg)
+    q, k, v = workload_bits(cfg)
+    qt, kt, vt = (mx.bf16_from_bits(x) for x in (q, k, v))
+    out = mx.forward(qt, kt, vt, mode)
+    torch.cuda.synchronize()
+    got_all = flat(mx.bits_from_bf16(out))
+    del out
+    codes = gpu_codes(mx, qt, kt, vt, mode)
+    del qt, kt, vt
+    torch.cuda.empty_cache()
+    BH = w.B * w.H
+    rows = full_size_rows(cfg)
+    got, ref, ref64, diag, head_of = [], [], [], [], []
+    for h in range(BH):
+        r, r64, dg = oracle_rows(codes, h, w.N, rows[h], mode, mx.kv_tile(), diag=True)
+        got.append(oracle.bf16_to_f64(got_all[h][rows[h]]))
+        ref.append(r)
+        ref64.append(r64)
+        diag.append(dg)
+        head_of.append(np.full(rows[h].size, h))
+    return dict(rows=rows, got=np.concatenate(got), ref=np.concatenate(ref), ref64=np.concatenate(ref64),
+                diag=np.concatenate(diag), head_of=np.concatenate(head_of))

@@ -170,3 +170,41 @@ def test_pnq_closes_gap_on_iid_data():
         gains[mode] = float(np.sum(out * ref) / np.sum(ref * ref))
     assert abs(gains["uos_pnq"] - 1) < abs(gains["ocp_vanilla"] - 1)
     assert abs(gains["uos_pnq"] - 1) < 0.1
+
+
+def _score_for(t: float, c32: np.float32) -> float:
+    """An fp32 score s whose fp32 product with c32 is exactly t (float32)."""
+    t32 = np.float32(t)
+    s = np.float32(t32 / c32)
+    for _ in range(64):
+        p = np.float32(np.float64(s) * np.float64(c32))
+        if p == t32:
+            return float(s)
+        s = np.nextafter(s, np.float32(np.inf) if p < t32 else np.float32(-np.inf))
+    raise AssertionError("no fp32 score for t")
+
+
+@pytest.mark.parametrize("rule,near_el,near_blk", [(UOS, 2, 1), (OCP, 2, 1)])
+def test_exponential_audit_counts_planted_cases(rule, near_el, near_blk):
+    """Diagnostic columns 6 and 7 count exactly the elements of P~ that sit
+    within 4 fp32 ulps of an E2M1 decision threshold (App. B midpoints) and
+    the blocks whose maximum sits within 4 ulps of an end of the scale
+    rule's range.  One query (d = 1, so c = log2 e) against planted scores:
+    block 0 holds the row maximum (t = 0, P~ = 1, sigma = 1/4 under both
+    rules), P~ = 2^-4 (normalized 0.25, a tie) and P~ ~ 0.1875 (normalized
+    0.75); block 1's maximum is ~ 7.25 * 2^-5 (the UOS boundary); block 2's is
+    2^-3 (the OCP boundary 4 sigma).  Every other score has t = -10."""
+    c32 = np.float32(1.4426950408889634)
+    t = np.full(72, -10.0)
+    t[0], t[1], t[2] = 0.0, -4.0, np.log2(0.1875)
+    t[32] = np.log2(7.25 * 2.0 ** -5)
+    t[64] = -3.0
+    k = np.array([[_score_for(x, c32)] for x in t])
+    q = np.ones((1, 1))
+    v = np.ones((72, 1))
+    _, dg = oracle.attention_rows(q, k, v, rule, 1, exact=0, block_c=128, diag=True)
+    assert dg.shape == (1, 8)
+    assert (dg[0, 6], dg[0, 7]) == (near_el, near_blk)
+    # the unquantized path has nothing to audit
+    _, dg = oracle.attention_rows(q, k, v, ID, 1, exact=0, block_c=128, diag=True)
+    assert (dg[0, 6], dg[0, 7]) == (0, 0)
