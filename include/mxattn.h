@@ -80,7 +80,8 @@ typedef enum {
 typedef enum {
     MXATTN_OK = 0,
     MXATTN_ERR_NULL = 1,        /* a required pointer is NULL              */
-    MXATTN_ERR_SHAPE = 2,       /* B, H or N < 1, or beyond a size limit    */
+    MXATTN_ERR_SHAPE = 2,       /* B, H or N < 1, beyond a size limit, or an
+                                   output that overlaps an input            */
     MXATTN_ERR_ALIGN = 3,       /* a pointer is not 16-byte aligned         */
     MXATTN_ERR_MODE = 4,        /* mode is not an mxattn_mode value         */
     MXATTN_ERR_AXIS = 5,        /* block_axis is not 2 or 3                 */
@@ -135,8 +136,8 @@ int mxattn_quantize_qmax(const void* x, uint8_t* codes, uint8_t* scales, int blo
  *   sse     device fp64 [B*H, nq], 8-byte aligned, written in full
  * Sums are formed in fp64 (each element's squared error exactly); the order
  * of additions within a workgroup is not fixed, so repeated calls may differ
- * in the last bits.  Uses stream-ordered workspace (hipMallocAsync on
- * `stream`): 2056 bytes per workgroup, about 2048 workgroups or one per
+ * in the last bits.  Uses stream-ordered workspace (the library's pool,
+ * see mxattn_release_workspace): 2056 bytes per workgroup, about 2048 workgroups or one per
  * (batch, head) if there are more, so about 2 KiB * max(B*H, 2048).
  * Returns MXATTN_OK, MXATTN_ERR_OOM, or another error status. */
 int mxattn_qmax_sse(const void* x, int block_axis, const double* qs, int nq, double* sse, int64_t B,
@@ -194,14 +195,15 @@ int mxattn_attention_rowsum_diag(const void* q, const void* k, int64_t B, int64_
 /* MXFP4 attention forward O = softmax(Q K^T / sqrt(d)) V with MXFP4 Q, K, V
  * and MXFP4 P~ (Algorithm 2, with its Hadamard rotation in mode
  * MXATTN_UOS_PNQ_ROT only; non-causal, no mask besides the sequence end).
- * Quantizes K along d and V along N into stream-ordered workspace
- * (hipMallocAsync/hipFreeAsync on `stream`, about 0.53 bytes per element of
- * each of K and V), then runs the fused kernel, which quantizes Q along d in
+ * Quantizes K along d and V along N into stream-ordered workspace (from
+ * the library's pool on `stream`, see mxattn_release_workspace; about 0.53
+ * bytes per element of each of K and V), then runs the fused kernel, which quantizes Q along d in
  * its prologue with codes bit-identical to mxattn_quantize's; in
  * MXATTN_UOS_PNQ_ROT, Q is rotated and quantized into the workspace first
  * (0.53 bytes per element more).
  *   q, k, v  device bf16 [B, H, N, d], 16-byte aligned
- *   out      device bf16 [B, H, N, d], 16-byte aligned, must not alias inputs
+ *   out      device bf16 [B, H, N, d], 16-byte aligned; MXATTN_ERR_SHAPE if
+ *            it shares a byte with q, k or v
  * Size limits (MXATTN_ERR_SHAPE otherwise): N <= 2^24 keys (the kernel
  * addresses one head's quantized K and V with 32-bit byte offsets) and
  * B * H * ceil(N / 128) <= 2^30 query tiles.
@@ -215,7 +217,8 @@ int mxattn_forward(const void* q, const void* k, const void* v, void* out, int64
  * of `mode` applies to the in-kernel quantization of P~; `mode` also selects
  * direct or PNQ placement.  All pointers are device pointers; code arrays
  * and `out` are 16-byte aligned, k_scales 4-byte aligned, the other scale
- * arrays may have any alignment. */
+ * arrays may have any alignment.  MXATTN_ERR_SHAPE if `out` shares a byte
+ * with any code or scale array. */
 int mxattn_attend(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
                   const uint8_t* k_scales, const uint8_t* v_codes, const uint8_t* v_scales,
                   void* out, int64_t B, int64_t H, int64_t N, int64_t d, int mode, void* stream);
@@ -253,6 +256,17 @@ const char* mxattn_status_string(int status);
 /* Detail of the last MXATTN_ERR_HIP or MXATTN_ERR_OOM on the calling
  * thread ("" if none). */
 const char* mxattn_last_error(void);
+
+/* Workspace.  mxattn_forward, mxattn_cross_forward, mxattn_attend,
+ * mxattn_cross_attend and mxattn_qmax_sse take their workspace, stream-
+ * ordered, from a memory pool that belongs to the library (one per device,
+ * created on first use; the device's default pool is left as it is).  The
+ * pool keeps freed workspace for the next call rather than returning it to
+ * the driver.  mxattn_release_workspace returns all of the current device's
+ * cached workspace that no call still uses; call it after the streams that
+ * ran the library's calls have completed, e.g. before a phase of a pipeline
+ * that needs the memory.  Returns MXATTN_OK or MXATTN_ERR_HIP. */
+int mxattn_release_workspace(void);
 
 /* ABI version (major * 100 + minor). */
 int mxattn_version(void);

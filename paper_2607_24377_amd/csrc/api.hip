@@ -1,10 +1,9 @@
 // api.hip -- the extern "C" entry points of libmxattn (see include/mxattn.h).
 //
 // Argument validation happens before any HIP call, so every error path is
-// free of device work.  The only global state is a once-per-device setting
-// of the stream-ordered allocator's release threshold (so the forward's
-// workspace is recycled by the pool instead of being returned to the driver
-// at every synchronization).
+// free of device work.  The only global state is the library's own
+// stream-ordered workspace pool per device (created once, see
+// workspace_alloc).
 #include <hip/hip_runtime.h>
 
 #include <atomic>
@@ -24,6 +23,12 @@ void set_error(const char* what, hipError_t e) {
 }
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+// Whether the byte ranges [a, a + na) and [b, b + nb) share a byte.
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return x < y + nb && y < x + na;
+}
 
 bool valid_mode(int mode) { return mode >= MXATTN_OCP_VANILLA && mode <= MXATTN_UOS_PNQ_ROT; }
 
@@ -46,25 +51,75 @@ int check_shape(int64_t B, int64_t H, int64_t N, int64_t d) {
 int rule_of(int mode) { return mode == MXATTN_OCP_VANILLA ? mxattn::kRuleOcp : mxattn::kRuleUos; }
 
 constexpr int kMaxDevices = 64;
-std::once_flag g_pool_once[kMaxDevices];
 
-void keep_pool_memory() {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return;
-    std::call_once(g_pool_once[dev], [dev] {
-        hipMemPool_t pool;
-        if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
-            uint64_t threshold = UINT64_MAX;
-            (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &threshold);
+// Workspace memory comes from a stream-ordered pool that belongs to the
+// library, one per device, created on first use.  Its release threshold has
+// no limit, so the forward's workspace is recycled between calls instead of
+// being returned to the driver at every synchronization; the device's
+// default pool, which other libraries share, keeps its attributes.
+// mxattn_release_workspace() hands the cached memory back.  If the pool
+// cannot be created, workspace comes from the default pool (unchanged).
+struct PoolSlot {
+    std::once_flag once;
+    std::atomic<hipMemPool_t> pool{nullptr};
+};
+PoolSlot g_pools[kMaxDevices];
+
+hipMemPool_t private_pool(int dev) {
+    if (dev < 0 || dev >= kMaxDevices) return nullptr;
+    PoolSlot& slot = g_pools[dev];
+    std::call_once(slot.once, [dev, &slot] {
+        hipMemPoolProps props{};
+        props.allocType = hipMemAllocationTypePinned;
+        props.handleTypes = hipMemHandleTypeNone;
+        props.location.type = hipMemLocationTypeDevice;
+        props.location.id = dev;
+        hipMemPool_t pool = nullptr;
+        if (hipMemPoolCreate(&pool, &props) != hipSuccess || !pool) {
+            (void)hipGetLastError();
+            return;
         }
+        uint64_t threshold = UINT64_MAX;
+        if (hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &threshold) != hipSuccess) {
+            (void)hipGetLastError();
+            (void)hipMemPoolDestroy(pool);
+            return;
+        }
+        slot.pool.store(pool);
     });
+    return slot.pool.load();
+}
+
+hipError_t workspace_alloc(void** p, size_t bytes, hipStream_t s) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return hipErrorInvalidDevice;
+    if (hipMemPool_t pool = private_pool(dev)) return hipMallocFromPoolAsync(p, bytes, pool, s);
+    return hipMallocAsync(p, bytes, s);
 }
 
 }  // namespace
 
 extern "C" {
 
-int mxattn_version(void) { return 100; }
+int mxattn_version(void) { return 101; }
+
+int mxattn_release_workspace(void) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) {
+        set_error("hipGetDevice", e);
+        return MXATTN_ERR_HIP;
+    }
+    if (dev < 0 || dev >= kMaxDevices) return MXATTN_OK;
+    hipMemPool_t pool = g_pools[dev].pool.load();
+    if (!pool) return MXATTN_OK;  // no workspace was ever taken on this device
+    e = hipMemPoolTrimTo(pool, 0);
+    if (e != hipSuccess) {
+        set_error("hipMemPoolTrimTo", e);
+        return MXATTN_ERR_HIP;
+    }
+    return MXATTN_OK;
+}
 
 int mxattn_kv_tile(void) { return mxattn::kKvTile; }
 
@@ -152,11 +207,10 @@ int mxattn_qmax_sse(const void* x, int block_axis, const double* qs, int nq, dou
     if (int st = check_shape(B, H, N, d)) return st;
     if (!aligned(x, 16) || !aligned(sse, 8)) return MXATTN_ERR_ALIGN;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    keep_pool_memory();
     void* ws = nullptr;
-    hipError_t e = hipMallocAsync(&ws, (size_t)mxattn::qmax_sse_workspace_bytes(block_axis, B * H, N), s);
+    hipError_t e = workspace_alloc(&ws, (size_t)mxattn::qmax_sse_workspace_bytes(block_axis, B * H, N), s);
     if (e != hipSuccess || !ws) {
-        set_error("hipMallocAsync", e);
+        set_error("workspace allocation", e);
         return MXATTN_ERR_OOM;
     }
     int st = MXATTN_OK;
@@ -312,6 +366,19 @@ static int launch_attend(const void* qraw, const uint8_t* qc, const uint8_t* qs,
     return MXATTN_OK;
 }
 
+// Whether `out` ([B, H, Nq, d] bf16) shares memory with any quantized operand.
+static bool attend_out_aliases(const uint8_t* qc, const uint8_t* qs, const uint8_t* kc, const uint8_t* ks,
+                               const uint8_t* vc, const uint8_t* vs, const void* out, int64_t B, int64_t H,
+                               int64_t Nq, int64_t Nkv, int64_t d) {
+    const size_t ob = (size_t)(B * H * Nq * d * 2);
+    return overlaps(out, ob, qc, mxattn_codes_bytes(MXATTN_AXIS_HEAD_DIM, B, H, Nq, d)) ||
+           overlaps(out, ob, qs, mxattn_scales_bytes(MXATTN_AXIS_HEAD_DIM, B, H, Nq, d)) ||
+           overlaps(out, ob, kc, mxattn_codes_bytes(MXATTN_AXIS_HEAD_DIM, B, H, Nkv, d)) ||
+           overlaps(out, ob, ks, mxattn_scales_bytes(MXATTN_AXIS_HEAD_DIM, B, H, Nkv, d)) ||
+           overlaps(out, ob, vc, mxattn_codes_bytes(MXATTN_AXIS_TOKENS, B, H, Nkv, d)) ||
+           overlaps(out, ob, vs, mxattn_scales_bytes(MXATTN_AXIS_TOKENS, B, H, Nkv, d));
+}
+
 int mxattn_cross_attend(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
                         const uint8_t* k_scales, const uint8_t* v_codes, const uint8_t* v_scales,
                         void* out, int64_t B, int64_t H, int64_t Nq, int64_t Nkv, int64_t d, int mode,
@@ -325,12 +392,13 @@ int mxattn_cross_attend(const uint8_t* q_codes, const uint8_t* q_scales, const u
     if (!aligned(q_codes, 16) || !aligned(k_codes, 16) || !aligned(v_codes, 16) ||
         !aligned(out, 16) || !aligned(k_scales, 4))
         return MXATTN_ERR_ALIGN;
+    if (attend_out_aliases(q_codes, q_scales, k_codes, k_scales, v_codes, v_scales, out, B, H, Nq, Nkv, d))
+        return MXATTN_ERR_SHAPE;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    keep_pool_memory();
     void* ws = nullptr;
-    hipError_t e = hipMallocAsync(&ws, (size_t)mxattn::tile_scales_bytes(B * H, Nkv), s);
+    hipError_t e = workspace_alloc(&ws, (size_t)mxattn::tile_scales_bytes(B * H, Nkv), s);
     if (e != hipSuccess || !ws) {
-        set_error("hipMallocAsync", e);
+        set_error("workspace allocation", e);
         return MXATTN_ERR_OOM;
     }
     int st = launch_attend(nullptr, q_codes, q_scales, k_codes, k_scales, v_codes, v_scales,
@@ -359,8 +427,12 @@ int mxattn_cross_forward(const void* q, const void* k, const void* v, void* out,
     if (int st = check_attention_shape(B, H, Nq, Nkv)) return st;
     if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16))
         return MXATTN_ERR_ALIGN;
+    {
+        const size_t ob = (size_t)(B * H * Nq * d * 2), kb = (size_t)(B * H * Nkv * d * 2);
+        if (overlaps(out, ob, q, ob) || overlaps(out, ob, k, kb) || overlaps(out, ob, v, kb))
+            return MXATTN_ERR_SHAPE;
+    }
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    keep_pool_memory();
 
     // Q is quantized in the attention kernel's prologue (bit-identical to the
     // head-dim quantizer), except for the rotated mode, whose Q is rotated
@@ -378,9 +450,9 @@ int mxattn_cross_forward(const void* q, const void* k, const void* v, void* out,
                          up(v_scales) + up(tiled);
 
     void* ws = nullptr;
-    hipError_t e = hipMallocAsync(&ws, total, s);
+    hipError_t e = workspace_alloc(&ws, total, s);
     if (e != hipSuccess || !ws) {
-        set_error("hipMallocAsync", e);
+        set_error("workspace allocation", e);
         return MXATTN_ERR_OOM;
     }
     uint8_t* p = static_cast<uint8_t*>(ws);

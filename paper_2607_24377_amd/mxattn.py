@@ -77,6 +77,8 @@ def lib() -> ctypes.CDLL:
             L.mxattn_status_string.restype = ctypes.c_char_p
             L.mxattn_last_error.argtypes = []
             L.mxattn_last_error.restype = ctypes.c_char_p
+            L.mxattn_release_workspace.argtypes = []
+            L.mxattn_release_workspace.restype = I
             L.mxattn_version.argtypes = []
             L.mxattn_version.restype = I
             _lib = L
@@ -279,3 +281,8 @@ def bf16_from_bits(bits, device="cuda") -> torch.Tensor:
 def bits_from_bf16(t: torch.Tensor):
     """numpy uint16 bit patterns of a bf16 tensor."""
     return t.detach().contiguous().cpu().view(torch.int16).numpy().view("uint16")
+
+
+def release_workspace():
+    """Return the current device's cached workspace (mxattn_release_workspace)."""
+    _check(lib().mxattn_release_workspace(), "mxattn_release_workspace")

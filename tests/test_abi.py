@@ -33,7 +33,7 @@ def test_header_declares_the_entry_points():
     for n in ["mxattn_quantize", "mxattn_forward", "mxattn_attend", "mxattn_codes_bytes",
               "mxattn_quantize_qmax", "mxattn_qmax_sse",
               "mxattn_scales_bytes", "mxattn_kv_tile", "mxattn_status_string",
-              "mxattn_last_error"]:
+              "mxattn_last_error", "mxattn_release_workspace"]:
         assert n in names
 
 
@@ -124,6 +124,32 @@ def test_forward_and_attend_reject_bad_arguments(L):
     bad = list(args)
     bad[1] = FAKE + 1  # q_scales may have any alignment: only the shape error fires
     assert a(*bad, 1, 1, 0, 128, 0, None) == 2
+
+
+def test_output_overlapping_an_input_is_rejected(L):
+    """`out` sharing a byte with an input is a shape error, caught before any
+    allocation or launch.  Only overlapping cases are called: the pointers
+    are not device memory."""
+    B, H, N, d = 1, 2, 64, 128
+    nb = B * H * N * d * 2  # bf16 bytes of one [B, H, N, d] tensor
+    q, k, v = FAKE, FAKE + (1 << 24), FAKE + (2 << 24)
+    f, c = L.mxattn_forward, L.mxattn_cross_forward
+    assert f(q, k, v, q, B, H, N, d, 2, None) == 2
+    assert f(q, k, v, q + nb - 16, B, H, N, d, 2, None) == 2   # last 16 bytes of q
+    assert f(q, k, v, k - nb + 16, B, H, N, d, 2, None) == 2   # first 16 bytes of k
+    assert f(q, k, v, v + 1024, B, H, N, d, 0, None) == 2
+    # cross-attention: out [B, H, Nq, d] against k, v [B, H, Nkv, d]
+    Nq, Nkv = 256, 16
+    assert c(q, k, v, k - B * H * Nq * d * 2 + 16, B, H, Nq, Nkv, d, 2, None) == 2
+    assert c(q, k, v, v + B * H * Nkv * d * 2 - 16, B, H, Nq, Nkv, d, 1, None) == 2
+    # quantized operands: codes and scales of Q, K and V
+    a, ca = L.mxattn_attend, L.mxattn_cross_attend
+    ops = [FAKE + (i << 24) for i in range(6)]  # qc, qs, kc, ks, vc, vs
+    for i in range(6):
+        assert a(*ops, ops[i], B, H, N, d, 2, None) == 2, i
+    qs_bytes = B * H * Nq * 4
+    assert ca(*ops, ops[1] - B * H * Nq * d * 2 + 16, B, H, Nq, Nkv, d, 2, None) == 2
+    assert ca(*ops, ops[1] + qs_bytes - 16, B, H, Nq, Nkv, d, 2, None) == 2
 
 
 def test_boundary_entry_points_reject_bad_arguments(L):

@@ -163,6 +163,8 @@ def test_attend_matches_forward_and_is_deterministic(mx):
     qt, kt, vt = (mx.bf16_from_bits(x) for x in (q, k, v))
     for mode in MODES:
         a = mx.forward(qt, kt, vt, mode)
+        torch.cuda.synchronize()
+        mx.release_workspace()  # the next call takes fresh workspace from the library's pool
         b = mx.forward(qt, kt, vt, mode)
         qc, qs = mx.quantize(qt, mx.AXIS_HEAD_DIM, mode)
         kc, ks = mx.quantize(kt, mx.AXIS_HEAD_DIM, mode)
