@@ -15,6 +15,30 @@ REL_L2_TOL = 2e-3
 MAX_ABS_TOL = 1e-2
 
 
+# A bf16 output element whose oracle (fp64) value lies within this relative
+# distance of the midpoint between two neighbouring bf16 values has two valid
+# roundings: the kernel takes that decision on an fp32 accumulation, the
+# oracle on fp64, so either neighbour is a correct result there.  The window
+# is 1/16 of bf16's half-ulp (2^-9 relative) and four times the largest
+# distance seen on the full-size workloads (2.5e-5).
+BF16_TIE_WINDOW = 2.0 ** -14
+
+
+def bf16_ties(got, ref, ref64):
+    """Boolean mask of elements where got and ref (bf16 values as fp64) are
+    the two bf16 neighbours of ref64 and ref64 lies within BF16_TIE_WINDOW
+    (relative) of their midpoint."""
+    got, ref, ref64 = (np.asarray(x, np.float64) for x in (got, ref, ref64))
+    lo, hi = np.minimum(got, ref), np.maximum(got, ref)
+    mid = 0.5 * (lo + hi)
+    neighbours = (got != ref) & (lo <= ref64) & (ref64 <= hi)
+    # lo and hi adjacent: no bf16 value strictly between them (bf16 = top 16
+    # bits of fp32, so adjacent values differ by one in those bits)
+    b = lambda x: (x.astype(np.float32).view(np.uint32) >> 16).astype(np.int64)
+    adjacent = np.abs(b(got) - b(ref)) == 1
+    return neighbours & adjacent & (np.abs(ref64 - mid) <= BF16_TIE_WINDOW * np.abs(ref64))
+
+
 def log(*a):
     print(*a, flush=True)
     sys.stdout.flush()

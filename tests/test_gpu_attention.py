@@ -10,8 +10,8 @@ import numpy as np
 import pytest
 
 import oracle
-from parity import (MAX_ABS_TOL, REL_L2_TOL, flat, full_size_sample, log, max_abs, oracle_rows,
-                    rel_l2, sample_rows, workload_bits)
+from parity import (MAX_ABS_TOL, REL_L2_TOL, bf16_ties, flat, full_size_sample, log, max_abs,
+                    oracle_rows, rel_l2, sample_rows, workload_bits)
 from paper_2607_24377_amd import inputs
 
 pytestmark = pytest.mark.gpu
@@ -87,7 +87,9 @@ def test_full_size_stratified_rows(mx, cfg, mode):
     """Full-size workloads in the launch the benchmark times, every mode, with
     the oracle on >= 2048 stratified rows spread over every head (first and
     ragged last query tile, the joint workload's text rows, random rows).
-    Each head, and the sample as a whole, must meet the tolerance.  The log
+    Each head, and the sample as a whole, must meet the tolerance; an element
+    whose oracle value sits at a bf16 rounding midpoint may take either
+    neighbouring bf16 value (bf16_ties).  The log
     gives the worst deviation and the oracle's audit of the exponential:
     P~ elements within 4 ulps of an E2M1 decision threshold and blocks whose
     maximum is within 4 ulps of a scale boundary, the only places where the
@@ -97,13 +99,23 @@ def test_full_size_stratified_rows(mx, cfg, mode):
     smp = full_size_sample(cfg, mode)
     g, r, hd = smp["got"], smp["ref"], smp["head_of"]
     assert np.all(np.isfinite(g))
-    rl, ma = rel_l2(g, r), max_abs(g, r)
+    # elements at a bf16 rounding midpoint (two valid roundings) are checked
+    # to be one of them; every other element is held to max-abs
+    ties = bf16_ties(g, r, smp["ref64"])
+    err = np.where(ties, 0.0, np.abs(g - r))
+    rl, ma = rel_l2(g, r), float(err.max())
     per_head = [rel_l2(g[hd == h], r[hd == h]) for h in range(w.B * w.H)]
-    worst_row = int(np.argmax(np.max(np.abs(g - r), axis=1)))
+    worst_row = int(np.argmax(err.max(axis=1)))
     near_el, near_blk = smp["diag"][:, 6].sum(), smp["diag"][:, 7].sum()
     log(f"[full] {w.name} mode={mode}: rows {g.shape[0]} over {w.B * w.H} heads, rel-L2 {rl:.3e}, "
         f"max-abs {ma:.3e} (head {hd[worst_row]}), worst head rel-L2 {max(per_head):.3e}; "
+        f"{int((g != r).sum())} elements differ from the oracle's bf16, {int(ties.sum())} of them "
+        f"rounding ties of fp32 vs fp64 (largest {np.abs(g - r)[ties].max() if ties.any() else 0:.3e}); "
         f"audit: {near_el:.0f} P~ near a threshold, {near_blk:.0f} blocks near a scale boundary")
+    for i, j in np.argwhere(ties)[:8]:
+        x = smp["ref64"][i, j]
+        log(f"[full]   tie: head {hd[i]} ch {j}: gpu {g[i, j]:.7g} oracle bf16 {r[i, j]:.7g} oracle fp64 "
+            f"{x:.12g}, {abs(x - (g[i, j] + r[i, j]) / 2) / abs(x):.2e} from the midpoint")
     assert rl <= REL_L2_TOL, (w.name, mode, rl)
     assert ma <= MAX_ABS_TOL, (w.name, mode, ma)
     assert max(per_head) <= REL_L2_TOL, (w.name, mode, int(np.argmax(per_head)), max(per_head))
