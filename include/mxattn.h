@@ -88,9 +88,11 @@ typedef enum {
     MXATTN_ERR_UNSUPPORTED = 6, /* d != 128                                 */
     MXATTN_ERR_OOM = 7,         /* workspace allocation failed              */
     MXATTN_ERR_HIP = 8,         /* a HIP call failed; see mxattn_last_error */
-    MXATTN_ERR_BOUNDARY = 9     /* a scale boundary q outside [4, 8], a
+    MXATTN_ERR_BOUNDARY = 9,    /* a scale boundary q outside [4, 8], a
                                    boundary count outside [1, 64], or a
                                    pre-scale gamma not in (0, 3e38)         */
+    MXATTN_ERR_SCRATCH = 10     /* the problem needs more than the static
+                                   scratch of mxattn_cross_attend_noalloc   */
 } mxattn_status;
 
 #define MXATTN_AXIS_TOKENS 2   /* blocks along N (V)      */
@@ -236,6 +238,28 @@ int mxattn_cross_attend(const uint8_t* q_codes, const uint8_t* q_scales, const u
                         const uint8_t* k_scales, const uint8_t* v_codes, const uint8_t* v_scales,
                         void* out, int64_t B, int64_t H, int64_t Nq, int64_t Nkv, int64_t d, int mode,
                         void* stream);
+
+/* mxattn_cross_attend without any allocation, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * and harnesses that forbid allocation.  Same arguments, checks and result
+ * as mxattn_cross_attend (bit-identical output, the same kernels); it calls
+ * no hipMalloc, hipMallocAsync, hipFree or any allocating routine.  Its one
+ * buffer beyond the inputs and `out`, the K^ and V^ scales rearranged into
+ * the kernel's operand order (1 KiB per (batch, head) and 128-key tile), is
+ * a static device array of MXATTN_NOALLOC_SCRATCH_BYTES that each device the
+ * library runs on holds until the process ends.  Limit: B * H * ceil(Nkv /
+ * 128) <= 32768 (e.g. H = 40 heads of up to 104 832 keys), else
+ * MXATTN_ERR_SCRATCH with a message in mxattn_last_error and nothing
+ * launched.  The array is fully rewritten by every call before it is read,
+ * but all calls on one device share it: calls that overlap in time on one
+ * device (different streams without ordering between them) race and give
+ * undefined results.  The first call on a device looks up the array's
+ * device address (hipGetSymbolAddress); MXATTN_ERR_HIP if that fails. */
+#define MXATTN_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+int mxattn_cross_attend_noalloc(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
+                                const uint8_t* k_scales, const uint8_t* v_codes, const uint8_t* v_scales,
+                                void* out, int64_t B, int64_t H, int64_t Nq, int64_t Nkv, int64_t d,
+                                int mode, void* stream);
 
 /* Sizes of the code and scale arrays of a [B, H, N, d] tensor blocked along
  * `block_axis`; 0 for invalid arguments. */

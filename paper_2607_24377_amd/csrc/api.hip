@@ -136,6 +136,7 @@ const char* mxattn_status_string(int s) {
         case MXATTN_ERR_UNSUPPORTED: return "unsupported head dimension (d must be 128)";
         case MXATTN_ERR_OOM: return "workspace allocation failed";
         case MXATTN_ERR_HIP: return "HIP runtime error";
+        case MXATTN_ERR_SCRATCH: return "problem too large for the static scratch of the no-allocation entry point (needs B*H*ceil(Nkv/128) <= 32768)";
         case MXATTN_ERR_BOUNDARY: return "invalid scale boundary (need 4 <= q <= 8 and 1 <= nq <= 64) or pre-scale (need 0 < gamma < 3e38)";
         default: return "unknown status";
     }
@@ -379,10 +380,11 @@ static bool attend_out_aliases(const uint8_t* qc, const uint8_t* qs, const uint8
            overlaps(out, ob, vs, mxattn_scales_bytes(MXATTN_AXIS_TOKENS, B, H, Nkv, d));
 }
 
-int mxattn_cross_attend(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
-                        const uint8_t* k_scales, const uint8_t* v_codes, const uint8_t* v_scales,
-                        void* out, int64_t B, int64_t H, int64_t Nq, int64_t Nkv, int64_t d, int mode,
-                        void* stream) {
+// Argument checks of the attention calls on quantized operands.
+static int check_attend_args(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
+                             const uint8_t* k_scales, const uint8_t* v_codes, const uint8_t* v_scales,
+                             const void* out, int64_t B, int64_t H, int64_t Nq, int64_t Nkv, int64_t d,
+                             int mode) {
     if (!q_codes || !q_scales || !k_codes || !k_scales || !v_codes || !v_scales || !out)
         return MXATTN_ERR_NULL;
     if (!valid_mode(mode)) return MXATTN_ERR_MODE;
@@ -394,6 +396,16 @@ int mxattn_cross_attend(const uint8_t* q_codes, const uint8_t* q_scales, const u
         return MXATTN_ERR_ALIGN;
     if (attend_out_aliases(q_codes, q_scales, k_codes, k_scales, v_codes, v_scales, out, B, H, Nq, Nkv, d))
         return MXATTN_ERR_SHAPE;
+    return MXATTN_OK;
+}
+
+int mxattn_cross_attend(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
+                        const uint8_t* k_scales, const uint8_t* v_codes, const uint8_t* v_scales,
+                        void* out, int64_t B, int64_t H, int64_t Nq, int64_t Nkv, int64_t d, int mode,
+                        void* stream) {
+    if (int st = check_attend_args(q_codes, q_scales, k_codes, k_scales, v_codes, v_scales, out, B, H, Nq, Nkv,
+                                   d, mode))
+        return st;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     void* ws = nullptr;
     hipError_t e = workspace_alloc(&ws, (size_t)mxattn::tile_scales_bytes(B * H, Nkv), s);
@@ -409,6 +421,77 @@ int mxattn_cross_attend(const uint8_t* q_codes, const uint8_t* q_scales, const u
         st = MXATTN_ERR_HIP;
     }
     return st;
+}
+
+// ---- the entry point that allocates nothing
+//
+// mxattn_cross_attend_noalloc keeps its one buffer beyond the inputs and the
+// output, the K^/V^ scales rearranged into MFMA operand order (1 KiB per
+// (batch, head) and 128-key tile), in this static device array instead of
+// allocated workspace.  Each device the library runs on holds its own copy
+// until the process ends.  On the host, `scratch` is only a stand-in symbol,
+// never a device address: the device address comes from hipGetSymbolAddress,
+// taken once per device with that device current, and only that address is
+// passed to kernels.  Every call on a device shares the device's array, so
+// calls that overlap in time on one device race.
+static __device__ __align__(256) uint8_t scratch[MXATTN_NOALLOC_SCRATCH_BYTES];
+
+struct ScratchSlot {
+    std::once_flag once;
+    hipError_t err = hipSuccess;
+    void* ptr = nullptr;
+};
+ScratchSlot g_scratch[kMaxDevices];
+
+// The current device's address of `scratch` (looked up on the first call on
+// that device).
+static int scratch_address(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) {
+        set_error("hipGetDevice", e);
+        return MXATTN_ERR_HIP;
+    }
+    if (dev < 0 || dev >= kMaxDevices) {
+        set_error("device index beyond the library's limit", hipErrorInvalidDevice);
+        return MXATTN_ERR_HIP;
+    }
+    ScratchSlot& slot = g_scratch[dev];
+    std::call_once(slot.once, [&slot] {
+        void* p = nullptr;
+        slot.err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (slot.err == hipSuccess && p)
+            slot.ptr = p;
+        else
+            (void)hipGetLastError();
+    });
+    if (slot.err != hipSuccess || !slot.ptr) {
+        set_error("hipGetSymbolAddress(scratch)", slot.err != hipSuccess ? slot.err : hipErrorInvalidSymbol);
+        return MXATTN_ERR_HIP;
+    }
+    *out = slot.ptr;
+    return MXATTN_OK;
+}
+
+int mxattn_cross_attend_noalloc(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,
+                                const uint8_t* k_scales, const uint8_t* v_codes, const uint8_t* v_scales,
+                                void* out, int64_t B, int64_t H, int64_t Nq, int64_t Nkv, int64_t d,
+                                int mode, void* stream) {
+    if (int st = check_attend_args(q_codes, q_scales, k_codes, k_scales, v_codes, v_scales, out, B, H, Nq, Nkv,
+                                   d, mode))
+        return st;
+    const int64_t need = mxattn::tile_scales_bytes(B * H, Nkv);
+    if (need > (int64_t)MXATTN_NOALLOC_SCRATCH_BYTES) {
+        std::snprintf(g_last_error, sizeof g_last_error,
+                      "mxattn_cross_attend_noalloc: %lld bytes of scale scratch needed (B*H*ceil(Nkv/128) KiB), "
+                      "the static buffer holds %lld",
+                      (long long)need, (long long)MXATTN_NOALLOC_SCRATCH_BYTES);
+        return MXATTN_ERR_SCRATCH;
+    }
+    void* sc = nullptr;
+    if (int st = scratch_address(&sc)) return st;
+    return launch_attend(nullptr, q_codes, q_scales, k_codes, k_scales, v_codes, v_scales, static_cast<uint8_t*>(sc),
+                         out, B, H, Nq, Nkv, mode, reinterpret_cast<hipStream_t>(stream));
 }
 
 int mxattn_attend(const uint8_t* q_codes, const uint8_t* q_scales, const uint8_t* k_codes,

@@ -64,6 +64,8 @@ def lib() -> ctypes.CDLL:
             L.mxattn_cross_forward.restype = I
             L.mxattn_cross_attend.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I64, I, P]
             L.mxattn_cross_attend.restype = I
+            L.mxattn_cross_attend_noalloc.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I64, I, P]
+            L.mxattn_cross_attend_noalloc.restype = I
             L.mxattn_attend.restype = I
             L.mxattn_codes_bytes.argtypes = [I, I64, I64, I64, I64]
             L.mxattn_codes_bytes.restype = SZ
