@@ -5,8 +5,8 @@
 // B_c) in increasing order, as Algorithm 2 does, and for each tile:
 //
 //   1. reads the tile's MXFP4 K^ and V^ codes and E8M0 scales from LDS (the
-//      next tile is already in flight into the other LDS buffer, copied by
-//      buffer loads straight into LDS);
+//      tiles after it are already in flight into the other LDS stages,
+//      copied by buffer loads straight into LDS);
 //   2. S^T = K^ Q^T on the block-scaled FP4 matrix cores
 //      (V_MFMA_SCALE_F32_32X32X64_F8F6F4, fp32 accumulation);
 //   3. online softmax in registers: running maximum m, correction
@@ -23,7 +23,11 @@
 //      second chunk's P~ is formed.
 //
 // After the last tile O = O~ / l is rounded to bf16 (Eq.
-// online_attention_output).
+// online_attention_output).  For long key sequences the steps of
+// consecutive tiles overlap (attention_pipelined_kernel: the score products
+// of tile j + 1 and the second PV chunk of tile j - 1 run during the softmax
+// of tile j); key sequences of at most four tiles stay in LDS for the whole
+// workgroup (attention_resident_kernel).
 //
 // Layouts chosen so that no lane shuffles are needed between the two
 // products: with S^T (keys as rows) each lane holds the scores of ONE query
@@ -60,7 +64,7 @@ constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr int kQw = 32;  // query rows per wave
 
-// LDS stage layout (bytes); two stages
+// LDS stage layout (bytes)
 constexpr int kKcOff = 0;      // K^ codes: 128 rows x 64 B, rows in MFMA order
 constexpr int kVcOff = 8192;   // V^ codes: 128 rows (channels) x 64 B (128 keys)
 constexpr int kKsOff = 16384;  // K^ scales: 64 lanes x 8 B, in MFMA operand order
@@ -133,7 +137,10 @@ struct TileLoader {
         }
     }
 
-    __device__ __forceinline__ void load(uint8_t* st, int tile) const {
+    __device__ __forceinline__ void load(uint8_t* st, int tile_) const {
+        // the tile index is wave-uniform; stating it keeps the offsets in
+        // scalar registers (a vector one would need a loop per load)
+        const int tile = __builtin_amdgcn_readfirstlane(tile_);
 #pragma unroll
         for (int it = 0; it < 2; it++) {
             __builtin_amdgcn_raw_ptr_buffer_load_lds(kc, (lds_ptr_t)(st + kKcOff + (2 * wave + it) * 1024), 16,
@@ -197,30 +204,25 @@ __device__ __forceinline__ uint32_t p_scale_byte(uint32_t mbits) {
     return (uint32_t)max(E - 2, 0);
 }
 
-// LDS reads issued as inline assembly.  The compiler does not see them as LDS
-// accesses, so it does not make them wait for the buffer-to-LDS loads of the
-// next tile (which it cannot tell apart from the stage being read); the reads'
-// completion is awaited by explicit s_waitcnt lgkmcnt statements that name
-// the destination registers.
+// LDS reads are ordinary loads from __shared__ arrays.  A lane reads its
+// 8-byte scale slot and the two 16-byte slots of row q of a stage (rows
+// 32 i + q share q's swizzle); every other row and region is an immediate
+// offset of the same per-lane address.
 typedef int v4i __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+struct LaneOff {
+    uint32_t sc, lo, hi;
+};
+__device__ __forceinline__ LaneOff lane_off(int q, int h, int lane) {
+    return {(uint32_t)(lane * 8), (uint32_t)(q * 64 + 16 * ((0 + h) ^ swz(q))),
+            (uint32_t)(q * 64 + 16 * ((2 + h) ^ swz(q)))};
 }
-// kOff is the instruction's 16-bit immediate byte offset, so one address
-// register per lane serves every read of a stage.
-template <int kOff = 0>
-__device__ __forceinline__ v4i lds_read128(uint32_t addr) {
-    static_assert(kOff >= 0 && kOff < 65536, "ds offset is 16 bits");
-    v4i r;
-    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(kOff));
-    return r;
+template <int kOff>
+__device__ __forceinline__ v4i ld128(const uint8_t* stage, uint32_t off) {
+    return *reinterpret_cast<const v4i*>(stage + kOff + off);
 }
-template <int kOff = 0>
-__device__ __forceinline__ uint2 lds_read64(uint32_t addr) {
-    static_assert(kOff >= 0 && kOff < 65536, "ds offset is 16 bits");
-    uint2 r;
-    asm volatile("ds_read_b64 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(kOff));
-    return r;
+template <int kOff>
+__device__ __forceinline__ uint2 ld64(const uint8_t* stage, uint32_t off) {
+    return *reinterpret_cast<const uint2*>(stage + kOff + off);
 }
 __device__ __forceinline__ v8i fp4_v(v4i x) {
     v8i r;
@@ -281,17 +283,6 @@ __device__ __forceinline__ uint32_t cvt_fp4x2(uint32_t old, float a, float b, fl
         case 2: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, a, b, scale, 2);
         default: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, a, b, scale, 3);
     }
-}
-
-// Per-lane LDS addresses of the stage at `st`: the lane's 8-byte scale slot
-// and the two 16-byte slots of row q (rows 32 i + q share q's swizzle); every
-// other row and region, and the second stage, are immediate offsets.
-struct LdsLane {
-    uint32_t sc, lo, hi;
-};
-__device__ __forceinline__ LdsLane lds_lane(const uint8_t* st, int q, int h, int lane) {
-    const uint32_t base = lds_addr(st);
-    return {base + lane * 8, base + q * 64 + 16 * ((0 + h) ^ swz(q)), base + q * 64 + 16 * ((2 + h) ^ swz(q))};
 }
 
 // The Q^ operands of S^T = K^ Q^T for one query row: lane (q, h) holds channel
@@ -363,48 +354,51 @@ __device__ __forceinline__ QOperands quantize_q(const QRaw& r) {
     return o;
 }
 
-// One KV tile of Algorithm 2 for the wave's 32 query rows, on LDS stage
-// kStage (relative to la): S^T = K^ Q^T, the online-softmax update of (m, l),
-// P^ and O~^T += V^T P^T.  Reads LDS only; the caller owns loads and barriers.
-// kFirst: the row's first tile, which sets m, l and O~ instead of updating
-// them (the rescale by alpha = 0 of a zero O~ and l is skipped, and the first
-// products accumulate onto zero), so they need no initial values.
-template <int kRule, bool kPnq, int kStage, bool kFirst = false>
-__device__ __forceinline__ void attend_tile(const LdsLane& la, int tile, int N, int h,
-                                            const QOperands& qo, const v8i& sel, float& m, RowSum& rs,
-                                            v16f (&O)[4]) {
-    const float cl = 0.12751743082459868f;  // fp32(log2(e) / sqrt(128))
-    constexpr int so = kStage * kStageBytes;
-    const v8i& qB0 = qo.b0;
-    const v8i& qB1 = qo.b1;
-    const int qS0 = qo.s0, qS1 = qo.s1;
-    const uint32_t a_sc = la.sc, a_lo = la.lo, a_hi = la.hi;
-    uint2 ksb = lds_read64<so + kKsOff>(a_sc);
-    uint2 vsb = lds_read64<so + kVsOff>(a_sc);
-
-    // ---- K^ operands for the 8 S products (chunk c, tile j, half hf):
-    // row 64 c + 32 j + q
-    v4i kr[2][2][2];
-    kr[0][0][0] = lds_read128<so + kKcOff + 0 * 2048>(a_lo);
-    kr[0][0][1] = lds_read128<so + kKcOff + 0 * 2048>(a_hi);
-    kr[0][1][0] = lds_read128<so + kKcOff + 1 * 2048>(a_lo);
-    kr[0][1][1] = lds_read128<so + kKcOff + 1 * 2048>(a_hi);
-    kr[1][0][0] = lds_read128<so + kKcOff + 2 * 2048>(a_lo);
-    kr[1][0][1] = lds_read128<so + kKcOff + 2 * 2048>(a_hi);
-    kr[1][1][0] = lds_read128<so + kKcOff + 3 * 2048>(a_lo);
-    kr[1][1][1] = lds_read128<so + kKcOff + 3 * 2048>(a_hi);
-    asm volatile("s_waitcnt lgkmcnt(0)"
-                 : "+v"(kr[0][0][0]), "+v"(kr[0][0][1]), "+v"(kr[0][1][0]), "+v"(kr[0][1][1]),
-                   "+v"(kr[1][0][0]), "+v"(kr[1][0][1]), "+v"(kr[1][1][0]), "+v"(kr[1][1][1]), "+v"(ksb),
-                   "+v"(vsb));
-    v8i kop[2][2][2];
+// Scores of keys at or past the end of the sequence set to -inf: S[c][jj][i]
+// is key 64 c + 16 jj + i past the lane's first key, `valid` keys of which
+// exist.  Whole-vector integer arithmetic, one bit-field select per score
+// (-inf's bits where the key index reaches the limit), so no per-score
+// condition masks are held in scalar registers.
+typedef int v16i __attribute__((ext_vector_type(16)));
+__device__ __forceinline__ void mask_tail(v16f (&S)[2][2], int valid) {
+    const v16i idx = {0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15};
 #pragma unroll
     for (int c = 0; c < 2; c++)
 #pragma unroll
-        for (int j = 0; j < 2; j++) {
-            kop[c][j][0] = fp4_v(kr[c][j][0]);
-            kop[c][j][1] = fp4_v(kr[c][j][1]);
+        for (int jj = 0; jj < 2; jj++) {
+            const v16i mk = ((valid - 1 - 64 * c - 16 * jj) - idx) >> 31;  // all ones past the end
+            const v16i b = __builtin_bit_cast(v16i, S[c][jj]);
+            S[c][jj] = __builtin_bit_cast(v16f, (mk & (int)0xFF800000u) | (~mk & b));
         }
+}
+
+// One KV tile of Algorithm 2 for the wave's 32 query rows, read from the LDS
+// stage at `st`: S^T = K^ Q^T, the online-softmax update of (m, l), P^ and
+// O~^T += V^T P^T.  Reads LDS only; the caller owns loads and barriers.
+// kFirst: the row's first tile, which sets m, l and O~ instead of updating
+// them (the rescale by alpha = 0 of a zero O~ and l is skipped, and the first
+// products accumulate onto zero), so they need no initial values.
+template <int kRule, bool kPnq, bool kFirst = false>
+__device__ __forceinline__ void attend_tile(const uint8_t* st, const LaneOff& lo, int tile, int N, int h,
+                                            const QOperands& qo, const v8i& sel, float& m, RowSum& rs,
+                                            v16f (&O)[4]) {
+    const float cl = 0.12751743082459868f;  // fp32(log2(e) / sqrt(128))
+    const v8i& qB0 = qo.b0;
+    const v8i& qB1 = qo.b1;
+    const int qS0 = qo.s0, qS1 = qo.s1;
+    const uint2 ksb = ld64<kKsOff>(st, lo.sc);
+    const uint2 vsb = ld64<kVsOff>(st, lo.sc);
+
+    // ---- K^ operands for the 8 S products (chunk c, tile j, half hf):
+    // row 64 c + 32 j + q
+    v8i kop[2][2][2];
+#pragma unroll
+    for (int c = 0; c < 2; c++) {
+        kop[c][0][0] = fp4_v(ld128<kKcOff + 0 * 2048>(st + 4096 * c, lo.lo));
+        kop[c][0][1] = fp4_v(ld128<kKcOff + 0 * 2048>(st + 4096 * c, lo.hi));
+        kop[c][1][0] = fp4_v(ld128<kKcOff + 1 * 2048>(st + 4096 * c, lo.lo));
+        kop[c][1][1] = fp4_v(ld128<kKcOff + 1 * 2048>(st + 4096 * c, lo.hi));
+    }
 
     // ---- S^T = K^ Q^T: S[c][j][i] is key 64c + 32h + 16j + i of the tile
     v16f S[2][2];
@@ -429,15 +423,12 @@ __device__ __forceinline__ void attend_tile(const LdsLane& la, int tile, int N, 
 
     // ---- V^ operands for the PV products (read now, used after softmax):
     // row (channel) 32 n + q
-    v4i vr[4][2];
-    vr[0][0] = lds_read128<so + kVcOff + 0 * 2048>(a_lo);
-    vr[0][1] = lds_read128<so + kVcOff + 0 * 2048>(a_hi);
-    vr[1][0] = lds_read128<so + kVcOff + 1 * 2048>(a_lo);
-    vr[1][1] = lds_read128<so + kVcOff + 1 * 2048>(a_hi);
-    vr[2][0] = lds_read128<so + kVcOff + 2 * 2048>(a_lo);
-    vr[2][1] = lds_read128<so + kVcOff + 2 * 2048>(a_hi);
-    vr[3][0] = lds_read128<so + kVcOff + 3 * 2048>(a_lo);
-    vr[3][1] = lds_read128<so + kVcOff + 3 * 2048>(a_hi);
+    v8i vop[4][2];
+#pragma unroll
+    for (int n = 0; n < 4; n++) {
+        vop[n][0] = fp4_v(ld128<kVcOff>(st + 2048 * n, lo.lo));
+        vop[n][1] = fp4_v(ld128<kVcOff>(st + 2048 * n, lo.hi));
+    }
 
     // ---- mask keys past the end of the sequence (last tile only)
     const int k0 = tile * 128;
@@ -461,18 +452,8 @@ __device__ __forceinline__ void attend_tile(const LdsLane& la, int tile, int N, 
     const float alpha = kFirst ? 0.f : __builtin_amdgcn_exp2f(m - m_new);  // 0 on the first tile
     m = m_new;
 
-    // ---- O~^T rescale and V^ operands, then per 64-key chunk: P~ -> P^ and
-    // that chunk's PV products (so chunk 0's products run under chunk 1's
-    // softmax)
-    asm volatile("s_waitcnt lgkmcnt(0)"
-                 : "+v"(vr[0][0]), "+v"(vr[0][1]), "+v"(vr[1][0]), "+v"(vr[1][1]), "+v"(vr[2][0]),
-                   "+v"(vr[2][1]), "+v"(vr[3][0]), "+v"(vr[3][1]));
-    v8i vop[4][2];
-#pragma unroll
-    for (int n = 0; n < 4; n++) {
-        vop[n][0] = fp4_v(vr[n][0]);
-        vop[n][1] = fp4_v(vr[n][1]);
-    }
+    // ---- O~^T rescale, then per 64-key chunk: P~ -> P^ and that chunk's PV
+    // products (so chunk 0's products run under chunk 1's softmax)
     if (!kFirst && __any(alpha != 1.f)) {
 #pragma unroll
         for (int n = 0; n < 4; n++)
@@ -621,79 +602,304 @@ __device__ __forceinline__ void store_rows(const AttnArgs& a, int64_t rowbase, i
     }
 }
 
+// ---------------------------------------------------------------------------
+// Long key sequences: the same tile computation, software-pipelined: the
+// score products of tile j + 1 are issued during the softmax of tile j (each
+// as soon as the score registers it overwrites have been consumed) and the
+// second PV chunk of a tile is deferred into the next one, so that no wave
+// waits for its own score products before its maximum and no LDS read sits
+// right before the product that consumes it.  On video720p this runs as fast
+// as a two-stage loop that issues each tile's score products as one group and
+// waits for them (the vector-ALU issue rate of the softmax bounds both), with
+// results identical bit for bit; it is kept because its LDS reads are
+// ordinary loads (see below) and its tail masking holds no per-score masks in
+// scalar registers.
+//
+// Per KV tile j of a wave (stage s = j mod 3 holds tile j's K^, V^ and scales):
+//   A  read tile j-1's chunk-1 V^ operands; block and row maxima of S(j),
+//      the running maximum and alpha.
+//   B  wait for tile j+1's loads, barrier, start tile j+2's loads (into the
+//      stage of tile j-1, read for the last time in A); tile j-1's deferred
+//      chunk-1 products (O~ += V^ P^ and the PNQ row sum) threaded through
+//      the first half of chunk 0's softmax; then the rescale of O~ and l by
+//      alpha.
+//   C  the rest of chunk 0, its products with V^ threaded through chunk 1's
+//      softmax, and the score products of tile j+1, each issued as soon as
+//      the score registers it overwrites have been consumed.
+// Every accumulator still receives its terms in the same order as in
+// attend_tile (O~: chunk 0 then chunk 1 of each tile, then the next tile's
+// rescale), so the results are identical.
+//
+// The three stages are separate LDS arrays read by ordinary loads, so the
+// compiler orders them against the buffer-to-LDS copies by their arrays
+// (a read of one stage never waits for the copies into another).
+constexpr int kPipeStages = 3;
+
+// The K^ operands of the score products of one tile in `stage`: rows
+// 64 c + 32 jj + q, channel blocks h (lo) and 2 + h (hi).
+struct KOperands {
+    v4i lo[2][2], hi[2][2];
+};
+__device__ __forceinline__ KOperands k_operands(const uint8_t* stage, const LaneOff& lo) {
+    KOperands k;
+    k.lo[0][0] = ld128<kKcOff + 0 * 2048>(stage, lo.lo);
+    k.hi[0][0] = ld128<kKcOff + 0 * 2048>(stage, lo.hi);
+    k.lo[0][1] = ld128<kKcOff + 1 * 2048>(stage, lo.lo);
+    k.hi[0][1] = ld128<kKcOff + 1 * 2048>(stage, lo.hi);
+    k.lo[1][0] = ld128<kKcOff + 2 * 2048>(stage, lo.lo);
+    k.hi[1][0] = ld128<kKcOff + 2 * 2048>(stage, lo.hi);
+    k.lo[1][1] = ld128<kKcOff + 3 * 2048>(stage, lo.lo);
+    k.hi[1][1] = ld128<kKcOff + 3 * 2048>(stage, lo.hi);
+    return k;
+}
+
+// The two score products of S[c][jj] (keys 64 c + 32 h + 16 jj + i of the
+// tile).
+template <int kC, int kJ>
+__device__ __forceinline__ v16f score_pair(const KOperands& k, const QOperands& qo, uint2 ksb) {
+    const int sreg = kC == 0 ? (int)ksb.x : (int)ksb.y;
+    const v16f zero = {};
+    v16f acc = mfma_fp4<2 * kJ>(fp4_v(k.lo[kC][kJ]), qo.b0, zero, sreg, qo.s0);
+    return mfma_fp4<2 * kJ + 1>(fp4_v(k.hi[kC][kJ]), qo.b1, acc, sreg, qo.s1);
+}
+
+// The V^ operands of chunk kC of a tile in `stage` (channel rows 32 n + q).
+struct VOperands {
+    v4i v[4];
+};
+template <int kC>
+__device__ __forceinline__ VOperands v_operands(const uint8_t* stage, const LaneOff& lo) {
+    const uint32_t off = kC == 0 ? lo.lo : lo.hi;
+    return {{ld128<kVcOff + 0 * 2048>(stage, off), ld128<kVcOff + 1 * 2048>(stage, off),
+             ld128<kVcOff + 2 * 2048>(stage, off), ld128<kVcOff + 3 * 2048>(stage, off)}};
+}
+
+// O~ += V^ P^ for chunk kC of a tile, and the PNQ row sum of that chunk.
+template <bool kPnq, int kC>
+__device__ __forceinline__ void pv_chunk(const VOperands& vo, const v8i& P, int psc, uint2 vsb, const v8i& sel,
+                                         RowSum& rs, v16f (&O)[4]) {
+    if (kPnq) rs.L = mfma16_fp4(sel, P, rs.L, 127, psc);
+    O[0] = mfma_fp4<kC>(fp4_v(vo.v[0]), P, O[0], (int)vsb.x, psc);
+    O[1] = mfma_fp4<2 + kC>(fp4_v(vo.v[1]), P, O[1], (int)vsb.x, psc);
+    O[2] = mfma_fp4<kC>(fp4_v(vo.v[2]), P, O[2], (int)vsb.y, psc);
+    O[3] = mfma_fp4<2 + kC>(fp4_v(vo.v[3]), P, O[3], (int)vsb.y, psc);
+}
+
+// P~ of one 32-key block (this lane's S[c][0] and S[c][1]) -> its E8M0 byte
+// and FP4 codes; the direct placement's row sum of P~ is added to lsum.
+template <int kRule, bool kPnq, int kHalf>
+__device__ __forceinline__ void softmax_half(const v16f& Sh, float m_new, float sf, uint32_t (&w)[4],
+                                             float& lsum) {
+    const float cl = 0.12751743082459868f;  // fp32(log2(e) / sqrt(128))
+#pragma unroll
+    for (int n = 0; n < 16; n += 2) {
+        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(Sh[n], cl, -m_new));
+        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(Sh[n + 1], cl, -m_new));
+        if (!kPnq) lsum += p0 + p1;
+        const int k = 16 * kHalf + n;  // key within the block
+        const uint32_t prev = (k & 7) == 0 ? __builtin_bit_cast(uint32_t, p0) : w[k >> 3];
+        w[k >> 3] = cvt_fp4x2(prev, p0, p1, sf, (k & 7) >> 1);
+    }
+}
+
+template <int kRule>
+__device__ __forceinline__ uint32_t block_scale(float bmax, float m_new) {
+    const float cl = 0.12751743082459868f;
+    const float mb = __builtin_amdgcn_exp2f(__builtin_fmaf(bmax, cl, -m_new));
+    return p_scale_byte<kRule>(__builtin_bit_cast(uint32_t, mb));
+}
+
+// State a wave carries from one KV tile to the next.
+struct PipeState {
+    v16f S[2][2];  // scores of the current tile
+    v16f O[4];
+    RowSum rs;
+    float m;
+    v8i P1;        // P^ of the previous tile's chunk 1 (its products are deferred)
+    int psc1;
+    uint2 vsb1;    // V^ scales of the previous tile
+};
+
+// Keeps the computation of its operands ahead of this point: an empty asm
+// statement that takes them as inputs (no instruction is emitted).  It stops
+// the compiler from sinking work past a branch into the block that uses it
+// (the exponentials of a chunk past the rescale branch, the next tile's score
+// products past the loop exit), which would regroup the products.  Operands
+// written by matrix-core products are named only to place the product's
+// issue, never read.
+template <typename T>
+__device__ __forceinline__ void pin_one(const T& x) {
+    asm volatile("" ::"v"(x));
+}
+template <typename... T>
+__device__ __forceinline__ void pin_here(const T&... x) {
+    (pin_one(x), ...);
+}
+
+// One KV tile j in stage kS: see the description above.  Stages kS + 1 and
+// kS + 2 (mod 3) hold tiles j + 1 and j - 1.
+template <int kRule, bool kPnq, int kS>
+__device__ __forceinline__ void pipe_tile(uint8_t* const (&stages)[kPipeStages], const TileLoader& loader,
+                                          const LaneOff& lo, int j, int ntiles, int N, int h, const QOperands& qo,
+                                          const v8i& sel, PipeState& ps) {
+    const float cl = 0.12751743082459868f;
+    const uint8_t* cur = stages[kS];
+    const uint8_t* nxt = stages[(kS + 1) % kPipeStages];
+    const uint8_t* prv = stages[(kS + 2) % kPipeStages];
+
+    // ---- A: tile j-1's chunk-1 V^ operands (its stage is reloaded after the
+    // barrier below), the maxima of S(j), the running maximum and alpha
+    const VOperands vprev = v_operands<1>(prv, lo);
+    const int k0 = j * 128;
+    if (k0 + 128 > N) mask_tail(ps.S, N - k0 - 32 * h);
+    float bmax[2];
+#pragma unroll
+    for (int c = 0; c < 2; c++) bmax[c] = block_max32(ps.S[c][0], ps.S[c][1]);
+    const float rmax = max_with_other_half(max2f(bmax[0], bmax[1]));
+    const float m_new = max2f(ps.m, mul_rd(cl, rmax));
+    const float alpha = __builtin_amdgcn_exp2f(ps.m - m_new);  // 0 on the first tile
+    ps.m = m_new;
+
+    // ---- B: tile j+1 landed everywhere, and every wave has read tile j-1's
+    // stage for the last time, so it takes tile j+2
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (j + 2 < ntiles) loader.load(stages[(kS + 2) % kPipeStages], j + 2);
+
+    // region 1: every LDS read of the rest of the tile; tile j-1's chunk-1
+    // products (on the first tile P^ = 0 with finite scales, which adds
+    // exactly zero) under chunk 0's first half.  After the last tile, the
+    // score products read a stage that holds an older tile (every stage is
+    // in bounds) and their results are unused: 8 products per query tile, in
+    // exchange for branch-free tile code.
+    const uint2 vsb = ld64<kVsOff>(cur, lo.sc);
+    const uint2 ksb = ld64<kKsOff>(nxt, lo.sc);
+    const KOperands kn = k_operands(nxt, lo);
+    const VOperands vc0 = v_operands<0>(cur, lo);
+    pv_chunk<kPnq, 1>(vprev, ps.P1, ps.psc1, ps.vsb1, sel, ps.rs, ps.O);
+    float lsum = 0.f;
+    uint32_t w0[4], w1[4];
+    const uint32_t sb0 = block_scale<kRule>(bmax[0], m_new);
+    const float sf0 = e8m0_as_f32(sb0);
+    softmax_half<kRule, kPnq, 0>(ps.S[0][0], m_new, sf0, w0, lsum);
+    pin_here(w0[0], w0[1], lsum, ps.O[0][0], ps.O[1][0], ps.O[2][0], ps.O[3][0], ps.rs.L[0], ksb, vsb, kn.lo[0][0],
+             kn.hi[0][0], kn.lo[0][1], kn.hi[0][1], kn.lo[1][0], kn.hi[1][0], kn.lo[1][1], kn.hi[1][1], vc0.v[0],
+             vc0.v[1], vc0.v[2], vc0.v[3]);
+
+    // the rescale of O~ and l by alpha follows the products above
+    if (__any(alpha != 1.f)) {
+#pragma unroll
+        for (int n = 0; n < 4; n++)
+#pragma unroll
+            for (int i = 0; i < 16; i++) ps.O[n][i] *= alpha;
+        if (kPnq) {
+            const uint32_t ab = __builtin_bit_cast(uint32_t, alpha);
+            const auto r = __builtin_amdgcn_permlane16_swap(ab, ab, false, false);
+            ps.rs.L[0] *= alpha;
+            ps.rs.L[1] *= __builtin_bit_cast(float, (uint32_t)r[1]);
+        }
+    }
+
+    // region 2: the rest of chunk 0, chunk 0's products, chunk 1, with the
+    // score products of tile j+1 issued as score registers become free
+    softmax_half<kRule, kPnq, 1>(ps.S[0][1], m_new, sf0, w0, lsum);
+    ps.S[0][0] = score_pair<0, 0>(kn, qo, ksb);
+    ps.S[0][1] = score_pair<0, 1>(kn, qo, ksb);
+    const v8i P0 = fp4_operand(make_uint4(w0[0], w0[1], w0[2], w0[3]));
+    pv_chunk<kPnq, 0>(vc0, P0, (int)sb0, vsb, sel, ps.rs, ps.O);
+    const uint32_t sb1 = block_scale<kRule>(bmax[1], m_new);
+    const float sf1 = e8m0_as_f32(sb1);
+    softmax_half<kRule, kPnq, 0>(ps.S[1][0], m_new, sf1, w1, lsum);
+    softmax_half<kRule, kPnq, 1>(ps.S[1][1], m_new, sf1, w1, lsum);
+    ps.S[1][0] = score_pair<1, 0>(kn, qo, ksb);
+    ps.S[1][1] = score_pair<1, 1>(kn, qo, ksb);
+    pin_here(ps.S[0][0][0], ps.S[0][1][0], ps.S[1][0][0], ps.S[1][1][0], ps.O[0][0], ps.O[1][0], ps.O[2][0],
+             ps.O[3][0]);
+    ps.P1 = fp4_operand(make_uint4(w1[0], w1[1], w1[2], w1[3]));
+    ps.psc1 = (int)sb1;
+    ps.vsb1 = vsb;
+    if (!kPnq) ps.rs.l = alpha * ps.rs.l + lsum;
+}
+
 template <int kRule, bool kPnq, bool kQraw>
-__global__ __launch_bounds__(kThreads, 2) void attention_kernel(AttnArgs a) {
-    __shared__ __attribute__((aligned(16))) uint8_t lds[2 * kStageBytes];
+__global__ __launch_bounds__(kThreads, 2) void attention_pipelined_kernel(AttnArgs a) {
+    __shared__ __attribute__((aligned(16))) uint8_t st0[kStageBytes];
+    __shared__ __attribute__((aligned(16))) uint8_t st1[kStageBytes];
+    __shared__ __attribute__((aligned(16))) uint8_t st2[kStageBytes];
+    uint8_t* const stages[kPipeStages] = {st0, st1, st2};
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lane = tid & 63;
     const int q = lane & 31, h = lane >> 5;
 
-    // XCD-aware order: consecutive workgroup ids go round-robin over the 8
-    // XCDs, so give each XCD a contiguous range of (head, query tile) work;
-    // the workgroups sharing an L2 then stream the same head's K^/V^.
     const int L = blockIdx.x;
     const int logical = (L & 7) * a.per_xcd + (L >> 3);
     if (logical >= a.total_tiles) return;
     const int bh = logical / a.qtiles;
     const int qt = logical - bh * a.qtiles;
-    const int N = a.N;    // keys (and values)
-    const int Nq = a.Nq;  // queries (= N for self-attention)
-    const int64_t rowbase = (int64_t)bh * Nq;  // Q^ and O rows of this head
+    const int N = a.N;
+    const int Nq = a.Nq;
+    const int64_t rowbase = (int64_t)bh * Nq;
     const int qi = qt * kQueryTile + wave * kQw + q;
     const int qic = min(qi, Nq - 1);
     const int ntiles = (N + 127) / 128;
 
     const TileLoader loader(a, bh, wave, lane);
-    loader.load(lds, 0);
+    loader.load(st0, 0);
+    if (ntiles > 1) loader.load(st1, 1);
 
-    // Q^ as the B operand of S^T = K^ Q^T
     QOperands qo;
     if constexpr (kQraw)
         qo = quantize_q<kRule>(q_raw(a, rowbase + qic, h));
     else
         qo = q_operands(a, rowbase + qic, h);
-
     const v8i sel = row_sum_selector(lane);
+    const LaneOff lo = lane_off(q, h, lane);
 
-    float m = -__builtin_inff();
-    RowSum rs;
-    rs.l = 0.f;
-    rs.L = v4f{0.f, 0.f, 0.f, 0.f};
-    v16f O[4];
+    PipeState ps;
+    ps.m = -__builtin_inff();
+    ps.rs.l = 0.f;
+    ps.rs.L = v4f{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int n = 0; n < 4; n++)
 #pragma unroll
-        for (int i = 0; i < 16; i++) O[n][i] = 0.f;
+        for (int i = 0; i < 16; i++) ps.O[n][i] = 0.f;
+    // the deferred products of "tile -1": P^ = 0 with finite scales
+    ps.P1 = v8i{};
+    ps.psc1 = 127;
+    ps.vsb1 = make_uint2(0x7F7F7F7Fu, 0x7F7F7F7Fu);
 
-    __builtin_amdgcn_s_waitcnt(0);  // direct LDS loads of tile 0 landed
+    __builtin_amdgcn_s_waitcnt(0);  // tiles 0 and 1 landed
     __syncthreads();
-
-    // two tiles per trip: stage 0 holds the even tiles, stage 1 the odd ones,
-    // so every LDS address is a lane register plus an immediate
-    const LdsLane la = lds_lane(lds, q, h, lane);
-    for (int tile = 0;; tile += 2) {
-        if (tile + 1 < ntiles) loader.load(lds + kStageBytes, tile + 1);
-        attend_tile<kRule, kPnq, 0>(la, tile, N, h, qo, sel, m, rs, O);
-        __builtin_amdgcn_s_waitcnt(0);  // the next tile's direct LDS loads landed
-        __syncthreads();
-        if (tile + 1 >= ntiles) break;
-
-        if (tile + 2 < ntiles) loader.load(lds, tile + 2);
-        attend_tile<kRule, kPnq, 1>(la, tile + 1, N, h, qo, sel, m, rs, O);
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-        if (tile + 2 >= ntiles) break;
+    {
+        const uint2 ksb = ld64<kKsOff>(st0, lo.sc);
+        const KOperands k0 = k_operands(st0, lo);
+        ps.S[0][0] = score_pair<0, 0>(k0, qo, ksb);
+        ps.S[0][1] = score_pair<0, 1>(k0, qo, ksb);
+        ps.S[1][0] = score_pair<1, 0>(k0, qo, ksb);
+        ps.S[1][1] = score_pair<1, 1>(k0, qo, ksb);
     }
+    for (int j = 0;; j += 3) {
+        pipe_tile<kRule, kPnq, 0>(stages, loader, lo, j, ntiles, N, h, qo, sel, ps);
+        if (j + 1 >= ntiles) break;
+        pipe_tile<kRule, kPnq, 1>(stages, loader, lo, j + 1, ntiles, N, h, qo, sel, ps);
+        if (j + 2 >= ntiles) break;
+        pipe_tile<kRule, kPnq, 2>(stages, loader, lo, j + 2, ntiles, N, h, qo, sel, ps);
+        if (j + 3 >= ntiles) break;
+    }
+    // the last tile's chunk-1 products (its stage is (ntiles - 1) mod 3)
+    const int last = (ntiles - 1) % kPipeStages;
+    pv_chunk<kPnq, 1>(v_operands<1>(last == 0 ? st0 : (last == 1 ? st1 : st2), lo), ps.P1, ps.psc1, ps.vsb1, sel,
+                      ps.rs, ps.O);
 
-    store_rows<kPnq>(a, rowbase, qi, q, h, lane, nullptr, false, rs, O);
+    store_rows<kPnq>(a, rowbase, qi, q, h, lane, nullptr, false, ps.rs, ps.O);
 }
 
 // Short key sequences (cross-attention over a text context, at most
 // kResidentKeys keys): the workgroup copies all of the head's K^ and V^ tiles
 // into LDS once and then runs several query tiles of that head against them,
 // with no per-tile loads or barriers; each query tile is the same computation
-// as in attention_kernel.
+// as in the streaming kernel.
 constexpr int kResidentTiles = kResidentKeys / 128;
 static_assert(kStagedStoreMaxTiles < kResidentTiles && kWaves * kOutStageBytes <= kStageBytes,
               "the output staging buffers fit in an unused tile slot");
@@ -725,6 +931,7 @@ __global__ __launch_bounds__(kThreads, 2) void attention_resident_kernel(AttnArg
     for (int t = 0; t < ntiles; t++) loader.load(lds + t * kStageBytes, t);
 
     const v8i sel = row_sum_selector(lane);
+    const LaneOff lo = lane_off(q, h, lane);
 
     __builtin_amdgcn_s_waitcnt(0);  // this wave's direct LDS loads landed
     __syncthreads();                // and every other wave's
@@ -765,10 +972,9 @@ __global__ __launch_bounds__(kThreads, 2) void attention_resident_kernel(AttnArg
         float m;
         RowSum rs;
         v16f O[4];
-        attend_tile<kRule, kPnq, 0, true>(lds_lane(lds, q, h, lane), 0, N, h, qo, sel, m, rs, O);
+        attend_tile<kRule, kPnq, true>(lds, lo, 0, N, h, qo, sel, m, rs, O);
         for (int tile = 1; tile < ntiles; tile++)
-            attend_tile<kRule, kPnq, 0>(lds_lane(lds + tile * kStageBytes, q, h, lane), tile, N, h, qo, sel, m,
-                                        rs, O);
+            attend_tile<kRule, kPnq>(lds + tile * kStageBytes, lo, tile, N, h, qo, sel, m, rs, O);
 
         const QOperands qn = operands(next);
         store_rows<kPnq>(a, rowbase, qi, q, h, lane, ostage, staged, rs, O);
@@ -838,9 +1044,9 @@ static void launch_attention_q(const AttnArgs& a, int mode, dim3 grid, hipStream
         return;
     }
     switch (mode) {
-        case 0: attention_kernel<kRuleOcp, false, kQraw><<<grid, kThreads, 0, stream>>>(a); break;
-        case 1: attention_kernel<kRuleUos, false, kQraw><<<grid, kThreads, 0, stream>>>(a); break;
-        default: attention_kernel<kRuleUos, true, kQraw><<<grid, kThreads, 0, stream>>>(a); break;
+        case 0: attention_pipelined_kernel<kRuleOcp, false, kQraw><<<grid, kThreads, 0, stream>>>(a); break;
+        case 1: attention_pipelined_kernel<kRuleUos, false, kQraw><<<grid, kThreads, 0, stream>>>(a); break;
+        default: attention_pipelined_kernel<kRuleUos, true, kQraw><<<grid, kThreads, 0, stream>>>(a); break;
     }
 }
 
