@@ -34,20 +34,32 @@ def log(msg: str):
     print(msg, file=sys.stderr, flush=True)
 
 
-def time_ms(fn, steps: int, warmup: int, torch) -> float:
-    """Average ms per call over `steps` calls after `warmup` calls, bracketed by
-    device synchronizations, timed with events on the current stream."""
+def time_steps(fn, steps: int, warmup: int, torch):
+    """Per-step times (ms) of `steps` calls after `warmup` untimed calls: the
+    timed calls are bracketed by device synchronizations and each is timed
+    between HIP events recorded on the current stream (the stream the
+    library launches on)."""
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    start.record()
-    for _ in range(steps):
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ev[0].record()
+    for i in range(steps):
         fn()
-    end.record()
+        ev[i + 1].record()
     torch.cuda.synchronize()
-    return start.elapsed_time(end) / steps
+    return [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+
+
+def median(xs):
+    xs = sorted(xs)
+    n = len(xs)
+    return xs[n // 2] if n % 2 else 0.5 * (xs[n // 2 - 1] + xs[n // 2])
+
+
+def time_ms(fn, steps: int, warmup: int, torch) -> float:
+    """Median ms per call (see time_steps)."""
+    return median(time_steps(fn, steps, warmup, torch))
 
 
 def measured_traffic(workload: str, mode: str):
@@ -102,10 +114,24 @@ def cpu_baseline(w, mode: str, rows_req: int, q_bits, k_bits, v_bits, block_c: i
             batch = min(8 * batch, 16384)
     rows = np.arange(done)
     flops = 4.0 * w.n_kv * w.d * rows.size
+    # the whole-tensor quantizer oracle: Q and K blocked along d, V along the
+    # keys, every element, with the mode's scale rule (and rotation)
+    rule = oracle.MODES[mode][0]
+    rot = mode in oracle.ROTATED
+    t0 = time.perf_counter()
+    oracle.quantize_rows(q_bits, rule, rotate=rot)
+    oracle.quantize_rows(k_bits, rule, rotate=rot)
+    oracle.quantize_keys(v_bits, rule)
+    qdt = time.perf_counter() - t0
+    elems = q_bits.size + k_bits.size + v_bits.size
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": nthreads, "kind": "oracle",
             "sample": f"{done} random query rows of head 0 of {w.name} ({mode}), all "
                       f"{w.n_kv} keys, fp64 tiled recurrence incl. dequantization; "
-                      f"{dt:.1f} s wall"}
+                      f"{dt:.1f} s wall",
+            "projected_forward_s": dt * (w.B * w.H * w.N) / done,
+            "quantizer": {"elements": elems, "seconds": qdt, "Melem_per_s": elems / qdt / 1e6,
+                          "GBps_equivalent": elems * 2.53125 / qdt / 1e9,
+                          "sample": f"every element of Q, K and V of {w.name}"}}
 
 
 def main():
@@ -162,7 +188,8 @@ def main():
         return lambda: mxattn.forward(q, k, v, mode, out=out)
 
     log(f"[bench] timing forward {args.mode}: warmup {args.warmup}, steps {args.steps}")
-    ms = time_ms(fwd(args.mode), args.steps, args.warmup, torch)
+    step_ms = time_steps(fwd(args.mode), args.steps, args.warmup, torch)
+    ms = median(step_ms)
     value = w.flops / (ms * 1e-3) / 1e12
 
     # the fused attention kernel alone (dominant kernel) on pre-quantized operands
@@ -179,6 +206,10 @@ def main():
     achieved = w.flops / (attn_ms * 1e-3) / 1e12
     elems = w.B * w.H * w.N * w.d
     extra = {
+        "timing": "median of per-step HIP-event times",
+        "ms_per_step_mean": sum(step_ms) / len(step_ms),
+        "ms_per_step_min": min(step_ms),
+        "ms_per_step_max": max(step_ms),
         "pct_of_mxfp4_peak": 100.0 * value / PEAK_FP4_TFLOPS,
         "attention_kernel_ms": attn_ms,
         "quantize_headdim_ms": quant_q_ms,

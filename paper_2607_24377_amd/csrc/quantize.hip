@@ -152,19 +152,22 @@ __global__ __launch_bounds__(256) void quantize_headdim_rot_kernel(const uint4* 
 }
 
 // ---------------------------------------------------------------------------
-// Blocks along the token axis (V).  A group of 128 tokens x 128 channels of
-// one head (32 KiB of bf16) is staged in LDS from coalesced 16-byte loads;
-// tokens past N are staged as +0 (the zero padding of the last block).  Wave w
-// then quantizes channel pairs 16w..16w+15 over the group's four 32-token
+// Blocks along the token axis (V).  A group of 256 tokens x 128 channels of
+// one head (64 KiB of bf16) is staged in LDS from coalesced 16-byte loads;
+// tokens past N are staged as +0 (the zero padding of the last block).  Wave
+// w of 8 then quantizes channel pairs 8w..8w+7 over the group's eight 32-token
 // blocks, lane (pair p, block b) owning one block of two channels.  Output
 // rows are tokens-contiguous per channel (16 code bytes and one scale byte per
-// (channel, 32-token block)), so the four lanes of a pair write the pair's 64
-// code bytes of this group contiguously.  A workgroup quantizes
-// kGroupsPerWg consecutive groups, loading the next group into registers
-// while the current one is quantized (two per workgroup measured fastest:
-// more leave too few workgroups to fill the chip evenly).
-constexpr int kVqTokens = 128;
-constexpr int kGroupsPerWg = 2;  // token groups per workgroup
+// (channel, 32-token block)), so the eight lanes of a pair write the pair's
+// 128 code bytes of this group, one whole 128-byte line per channel row, in
+// one store instruction.  (Groups of 128 tokens wrote half lines, 64 bytes
+// into each of 128 rows far apart, and took 5 % longer.)  The code may
+// quantize kGroupsPerWg consecutive groups per workgroup, loading the next
+// group into registers while the current one is quantized; one group per
+// workgroup measured fastest with 256-token groups.
+constexpr int kVqTokens = 256;
+constexpr int kVqThreads = 512;
+constexpr int kGroupsPerWg = 1;  // token groups per workgroup
 
 // Two bf16 values (a packed pair) to FP4 codes divided by `scale`, into byte
 // `sel` of `old` (the conversion takes the byte index as an immediate).
@@ -179,14 +182,14 @@ __device__ __forceinline__ uint32_t cvt_fp4x2_bf16(uint32_t old, uint32_t pair, 
 }
 
 template <int kRule>
-__global__ __launch_bounds__(256) void quantize_tokens_kernel(const uint4* __restrict__ x,
+__global__ __launch_bounds__(kVqThreads) void quantize_tokens_kernel(const uint4* __restrict__ x,
                                                               uint8_t* __restrict__ codes,
                                                               uint8_t* __restrict__ scales, int N,
                                                               int nb, int groups, int per_xcd, int total,
                                                               Boundary bq) {
-    // [token][64 dwords = 128 bf16]; the 32-token quarter q of the group is
-    // stored with its dword columns XOR-ed by 16 q, so that the four lanes
-    // reading the same channel pair in four quarters hit four bank groups
+    // [token][64 dwords = 128 bf16]; the 32-token block b of the group is
+    // stored with its dword columns XOR-ed by 8 b, so that the eight lanes
+    // reading the same channel pair in eight blocks hit eight bank groups
     __shared__ uint32_t tile[kVqTokens * 64];
     const int tid = threadIdx.x;
     // consecutive workgroup ids go round-robin over the 8 XCDs: give each XCD
@@ -205,7 +208,7 @@ __global__ __launch_bounds__(256) void quantize_tokens_kernel(const uint4* __res
         const uint4* src = x + (int64_t)bh * N * 16;
 #pragma unroll
         for (int k = 0; k < 8; k++) {
-            const int ch = tid + 256 * k;
+            const int ch = tid + kVqThreads * k;
             const int tok = ch >> 4, part = ch & 15;
             r[k] = (g * kVqTokens + tok < N) ? nt_load(src + (int64_t)(g * kVqTokens + tok) * 16 + part)
                                              : make_uint4(0, 0, 0, 0);
@@ -217,27 +220,27 @@ __global__ __launch_bounds__(256) void quantize_tokens_kernel(const uint4* __res
         __syncthreads();  // the previous group's LDS reads are done
 #pragma unroll
         for (int k = 0; k < 8; k++) {
-            const int ch = tid + 256 * k;
+            const int ch = tid + kVqThreads * k;
             const int tok = ch >> 4, part = ch & 15;
-            *reinterpret_cast<uint4*>(&tile[tok * 64 + ((part * 4) ^ (16 * (tok >> 5)))]) = buf[k];
+            *reinterpret_cast<uint4*>(&tile[tok * 64 + ((part * 4) ^ (8 * (tok >> 5)))]) = buf[k];
         }
         __syncthreads();
         if (lg + 1 < last) fetch(lg + 1, buf);  // in flight while this group is quantized
         const int bh = lg / groups, g = lg % groups;
 
-        // wave w: channel pairs 16 w .. 16 w + 15; lane: pair p = lane / 4, token
-        // block b = lane % 4 of the group.  The four lanes of a pair write the
-        // pair's four 16-byte code chunks of this group next to each other.
+        // wave w: channel pairs 8 w .. 8 w + 7; lane: pair p = lane / 8, token
+        // block b = lane % 8 of the group.  The eight lanes of a pair write the
+        // pair's eight 16-byte code chunks of this group next to each other.
         const int w = tid >> 6, lane = tid & 63;
-        const int p = lane >> 2, b = lane & 3;
-        const int cp = 16 * w + p;  // channels 2cp, 2cp+1 (dword column cp)
-        const int blk = 4 * g + b;
+        const int p = lane >> 3, b = lane & 7;
+        const int cp = 8 * w + p;  // channels 2cp, 2cp+1 (dword column cp)
+        const int blk = 8 * g + b;
         if (blk < nb) {
             uint32_t col[32];
             uint32_t m0 = 0, m1 = 0;
 #pragma unroll
             for (int t = 0; t < 32; t++) {
-                uint32_t d = tile[(32 * b + t) * 64 + (cp ^ (16 * b))];
+                uint32_t d = tile[(32 * b + t) * 64 + (cp ^ (8 * b))];
                 col[t] = d;
                 m0 = max(m0, d & 0x7FFFu);
                 m1 = max(m1, (d >> 16) & 0x7FFFu);
@@ -315,13 +318,13 @@ hipError_t launch_quantize_tokens(const void* x, uint8_t* codes, uint8_t* scales
     const dim3 grid((unsigned)(8 * per_xcd));
     const Boundary bq = boundary_of(rule == kRuleQmax ? qmax : 7.25);
     if (rule == kRuleUos)
-        quantize_tokens_kernel<kRuleUos><<<grid, 256, 0, stream>>>((const uint4*)x, codes, scales,
+        quantize_tokens_kernel<kRuleUos><<<grid, kVqThreads, 0, stream>>>((const uint4*)x, codes, scales,
                                                                     (int)N, nb, groups, per_xcd, total, bq);
     else if (rule == kRuleQmax)
-        quantize_tokens_kernel<kRuleQmax><<<grid, 256, 0, stream>>>((const uint4*)x, codes, scales,
+        quantize_tokens_kernel<kRuleQmax><<<grid, kVqThreads, 0, stream>>>((const uint4*)x, codes, scales,
                                                                      (int)N, nb, groups, per_xcd, total, bq);
     else
-        quantize_tokens_kernel<kRuleOcp><<<grid, 256, 0, stream>>>((const uint4*)x, codes, scales,
+        quantize_tokens_kernel<kRuleOcp><<<grid, kVqThreads, 0, stream>>>((const uint4*)x, codes, scales,
                                                                     (int)N, nb, groups, per_xcd, total, bq);
     return hipGetLastError();
 }
