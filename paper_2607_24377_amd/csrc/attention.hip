@@ -768,7 +768,12 @@ __device__ __forceinline__ void pipe_tile(uint8_t* const (&stages)[kPipeStages],
 
     // region 1: every LDS read of the rest of the tile; tile j-1's chunk-1
     // products (on the first tile P^ = 0 with finite scales, which adds
-    // exactly zero) under chunk 0's first half.  After the last tile, the
+    // exactly zero) under chunk 0's first half, then the first score
+    // products of tile j+1 into the registers that half freed.  Each score
+    // pair of tile j+1 is issued as soon as the softmax has consumed the
+    // scores it overwrites, which spreads the products evenly over the
+    // tile's vector work (issuing them in two groups of four was slower).
+    // After the last tile, the
     // score products read a stage that holds an older tile (every stage is
     // in bounds) and their results are unused: 8 products per query tile, in
     // exchange for branch-free tile code.
@@ -782,9 +787,10 @@ __device__ __forceinline__ void pipe_tile(uint8_t* const (&stages)[kPipeStages],
     const uint32_t sb0 = block_scale<kRule>(bmax[0], m_new);
     const float sf0 = e8m0_as_f32(sb0);
     softmax_half<kRule, kPnq, 0>(ps.S[0][0], m_new, sf0, w0, lsum);
-    pin_here(w0[0], w0[1], lsum, ps.O[0][0], ps.O[1][0], ps.O[2][0], ps.O[3][0], ps.rs.L[0], ksb, vsb, kn.lo[0][0],
-             kn.hi[0][0], kn.lo[0][1], kn.hi[0][1], kn.lo[1][0], kn.hi[1][0], kn.lo[1][1], kn.hi[1][1], vc0.v[0],
-             vc0.v[1], vc0.v[2], vc0.v[3]);
+    ps.S[0][0] = score_pair<0, 0>(kn, qo, ksb);
+    pin_here(ps.S[0][0][0], w0[0], w0[1], lsum, ps.O[0][0], ps.O[1][0], ps.O[2][0], ps.O[3][0], ps.rs.L[0], ksb,
+             vsb, kn.lo[0][0], kn.hi[0][0], kn.lo[0][1], kn.hi[0][1], kn.lo[1][0], kn.hi[1][0], kn.lo[1][1],
+             kn.hi[1][1], vc0.v[0], vc0.v[1], vc0.v[2], vc0.v[3]);
 
     // the rescale of O~ and l by alpha follows the products above
     if (__any(alpha != 1.f)) {
@@ -803,15 +809,15 @@ __device__ __forceinline__ void pipe_tile(uint8_t* const (&stages)[kPipeStages],
     // region 2: the rest of chunk 0, chunk 0's products, chunk 1, with the
     // score products of tile j+1 issued as score registers become free
     softmax_half<kRule, kPnq, 1>(ps.S[0][1], m_new, sf0, w0, lsum);
-    ps.S[0][0] = score_pair<0, 0>(kn, qo, ksb);
     ps.S[0][1] = score_pair<0, 1>(kn, qo, ksb);
     const v8i P0 = fp4_operand(make_uint4(w0[0], w0[1], w0[2], w0[3]));
     pv_chunk<kPnq, 0>(vc0, P0, (int)sb0, vsb, sel, ps.rs, ps.O);
     const uint32_t sb1 = block_scale<kRule>(bmax[1], m_new);
     const float sf1 = e8m0_as_f32(sb1);
     softmax_half<kRule, kPnq, 0>(ps.S[1][0], m_new, sf1, w1, lsum);
-    softmax_half<kRule, kPnq, 1>(ps.S[1][1], m_new, sf1, w1, lsum);
     ps.S[1][0] = score_pair<1, 0>(kn, qo, ksb);
+    pin_here(ps.S[1][0][0], w1[0], w1[1]);
+    softmax_half<kRule, kPnq, 1>(ps.S[1][1], m_new, sf1, w1, lsum);
     ps.S[1][1] = score_pair<1, 1>(kn, qo, ksb);
     pin_here(ps.S[0][0][0], ps.S[0][1][0], ps.S[1][0][0], ps.S[1][1][0], ps.O[0][0], ps.O[1][0], ps.O[2][0],
              ps.O[3][0]);
