@@ -134,6 +134,98 @@ def cpu_baseline(w, mode: str, rows_req: int, q_bits, k_bits, v_bits, block_c: i
                           "sample": f"every element of Q, K and V of {w.name}"}}
 
 
+def stratified_rows(N: int, n_heads: int, per_head: int, seed: int, text_tokens: int = 0, tile: int = 128):
+    """{head: query rows} of a bounded oracle sample: rows of the first query
+    tile, of the ragged last query tile and the sequence's end, each head's
+    share of the text rows, and random rows, per_head rows per head."""
+    import numpy as np
+
+    out = {}
+    last = (N - 1) // tile * tile
+    for h in range(n_heads):
+        rng = np.random.default_rng(seed + h)
+        rows = {r for r in (0, 1, 63, 127, last, last + 1, N - 2, N - 1) if 0 <= r < N}
+        if text_tokens:
+            rows |= set(range(N - text_tokens + h, N, n_heads))
+        while len(rows) < min(per_head, N):
+            rows.add(int(rng.integers(N)))
+        out[h] = np.array(sorted(rows), dtype=np.int64)
+    return out
+
+
+def cpu_table(modes, sample_rows: int, steps: int, warmup: int):
+    """The CPU oracle per configuration, beside the GPU forward of the same
+    configuration and mode: the quantizer oracle over every element of Q, K
+    and V, and the attention oracle on every row of the two small workloads
+    and on about `sample_rows` rows spread over every head of the long ones,
+    projected to the whole problem.  One JSON line per (workload, mode)."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2607_24377_amd import inputs, mxattn
+
+    dev = torch.device("cuda:0")
+    nthreads = oracle.threads(0)
+    for w in inputs.WORKLOADS:
+        log(f"[cpu-table] generating {w.name}")
+        q_bits, k_bits, v_bits = inputs.generate(w)
+        q, k, v = (mxattn.bf16_from_bits(x, dev) for x in (q_bits, k_bits, v_bits))
+        out = torch.empty_like(q)
+        bh = w.B * w.H
+        if w.flops < 1e12:  # every row
+            sample = {h: np.arange(w.N, dtype=np.int64) for h in range(bh)}
+        else:
+            sample = stratified_rows(w.N, bh, -(-sample_rows // bh), 7, w.text_tokens)
+        nrows = sum(r.size for r in sample.values())
+        for mode in modes:
+            log(f"[cpu-table] {w.name} {mode}: GPU forward")
+            short = w.flops < 1e13
+            gpu_ms = time_ms(lambda: mxattn.forward(q, k, v, mode, out=out), max(steps, 100 if short else steps),
+                             max(warmup, 20 if short else warmup), torch)
+            log(f"[cpu-table] {w.name} {mode}: oracle quantizer, every element")
+            rule = oracle.MODES[mode][0]
+            rot = mode in oracle.ROTATED
+            t0 = time.perf_counter()
+            qc, qs = oracle.quantize_rows(q_bits, rule, rotate=rot)
+            kc, ks = oracle.quantize_rows(k_bits, rule, rotate=rot)
+            vc, vs = oracle.quantize_keys(v_bits, rule)
+            qdt = time.perf_counter() - t0
+            flat = lambda a: a.reshape((-1,) + a.shape[2:])
+            qc, qs, kc, ks, vc, vs = (flat(a) for a in (qc, qs, kc, ks, vc, vs))
+            log(f"[cpu-table] {w.name} {mode}: oracle attention, {nrows} rows over {bh} heads")
+            # per head: dequantize K^, V^ (a cost per head, not per row), then
+            # the tiled recurrence for the sampled rows (a cost per row)
+            p_rule, pnq = oracle.MODES[mode]
+            ddt = adt = 0.0
+            for h, rows in sample.items():
+                t0 = time.perf_counter()
+                qh = oracle.dequant_rows(np.ascontiguousarray(qc[h][rows]), np.ascontiguousarray(qs[h][rows]))
+                kh = oracle.dequant_rows(kc[h], ks[h])
+                vh = oracle.dequant_keys(vc[h], vs[h], w.n_kv)
+                t1 = time.perf_counter()
+                oracle.attention_rows(qh, kh, vh, p_rule, pnq, 0, mxattn.kv_tile())
+                ddt += t1 - t0
+                adt += time.perf_counter() - t1
+            elems = q_bits.size + k_bits.size + v_bits.size
+            proj = ddt + adt * (bh * w.N) / nrows
+            print(json.dumps({
+                "workload": w.name, "B": w.B, "H": w.H, "N": w.N, "mode": mode, "cores": nthreads,
+                "gpu_forward_ms": gpu_ms,
+                "oracle_quantizer": {"elements": elems, "seconds": qdt, "Melem_per_s": elems / qdt / 1e6,
+                                     "GBps_equivalent": elems * 2.53125 / qdt / 1e9},
+                "oracle_attention": {"rows": nrows, "all_rows": nrows == bh * w.N, "seconds": adt,
+                                     "dequantize_seconds": ddt,
+                                     "rows_per_s": nrows / adt,
+                                     "score_elements_per_s": nrows * w.n_kv / adt,
+                                     "TFLOPs": 4.0 * w.n_kv * w.d * nrows / adt / 1e12,
+                                     "projected_full_s": proj},
+                "oracle_over_gpu": proj * 1e3 / gpu_ms,
+            }), flush=True)
+        del q, k, v, out
+        torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -148,6 +240,10 @@ def main():
                     help="skip the boundary-sweep and row-sum diagnostic timings")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--cpu-table", action="store_true",
+                    help="instead of the bench line: the CPU oracle per workload and mode beside the GPU "
+                         "forward (one JSON line each)")
+    ap.add_argument("--cpu-table-rows", type=int, default=2048)
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -165,6 +261,10 @@ def main():
         sys.exit(1)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.cpu_table:
+        mxattn.lib()
+        cpu_table(["ocp_vanilla", "uos", "uos_pnq"], args.cpu_table_rows, args.steps or 10, args.warmup or 3)
+        return
     w = inputs.workload(args.workload)
     log(f"[bench] generating {w.name} B={w.B} H={w.H} N={w.N} d={w.d}")
     q_bits, k_bits, v_bits = inputs.generate(w)
