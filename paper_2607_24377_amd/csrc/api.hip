@@ -347,15 +347,18 @@ static int launch_attend(const void* qraw, const uint8_t* qc, const uint8_t* qs,
     a.Nq = (int)Nq;
     a.nb = (int)((Nkv + 31) / 32);
     a.qtiles = (int)((Nq + mxattn::kQueryTile - 1) / mxattn::kQueryTile);
-    // one query tile per workgroup; with K^/V^ resident in LDS, as many as
-    // keep about 1024 workgroups (4 per CU) busy, at most 16
-    int64_t qpw = 1;
+    // one query tile per workgroup; with K^/V^ resident in LDS, chunks of at
+    // most 16 query tiles, as many as fill whole rounds of the 512 workgroups
+    // resident at once (two per CU), split evenly by the kernel
+    int64_t nchunks = a.qtiles;
     if (Nkv <= mxattn::kResidentKeys) {
-        qpw = B * H * a.qtiles / 1024;
-        qpw = qpw < 1 ? 1 : (qpw > 16 ? 16 : qpw);
+        const int64_t slots = 512, bh = B * H;
+        const int64_t min_chunks = (a.qtiles + 15) / 16;
+        const int64_t rounds = (bh * min_chunks + slots - 1) / slots;
+        const int64_t k = rounds * slots / bh;
+        nchunks = k < min_chunks ? min_chunks : (k > a.qtiles ? a.qtiles : k);
     }
-    a.qt_per_wg = (int)qpw;
-    a.nchunks = (int)((a.qtiles + qpw - 1) / qpw);
+    a.nchunks = (int)nchunks;
     const int64_t total = B * H * a.nchunks;
     a.total_tiles = (int)total;
     a.per_xcd = (int)((total + 7) / 8);

@@ -41,8 +41,8 @@
 // 3-way max per score) costs about twice the matrix-core time of the two
 // products, so the kernel is bound by vector-ALU issue; two workgroups per CU
 // give each SIMD two waves, whose matrix-core work overlaps the other's
-// softmax (not for free: vector instructions issue 30-45 % slower while an
-// FP4 MFMA executes).
+// softmax (not for free: vector instructions issue about a third slower
+// while another wave's FP4 32x32x64 products execute).
 //
 // Arithmetic contract (mirrored by the CPU oracle):
 //   s     fp32 accumulation of exact FP4 products (matrix core)
@@ -923,8 +923,9 @@ __global__ __launch_bounds__(kThreads, 2) void attention_resident_kernel(AttnArg
     if (logical >= a.total_tiles) return;
     const int bh = logical / a.nchunks;
     const int chunk = logical - bh * a.nchunks;
-    const int qt0 = chunk * a.qt_per_wg;
-    const int qt1 = min(a.qtiles, qt0 + a.qt_per_wg);
+    // the head's query tiles split as evenly as possible over nchunks
+    const int qt0 = (int)((int64_t)chunk * a.qtiles / a.nchunks);
+    const int qt1 = (int)((int64_t)(chunk + 1) * a.qtiles / a.nchunks);
     const int N = a.N;
     const int Nq = a.Nq;
     const int64_t rowbase = (int64_t)bh * Nq;

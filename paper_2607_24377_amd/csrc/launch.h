@@ -50,7 +50,6 @@ struct AttnArgs {
     int qtiles;
     int total_tiles;    // workgroups that do work
     int per_xcd;
-    int qt_per_wg;      // resident kernel: query tiles per workgroup
     int nchunks;        // resident kernel: workgroups per (batch, head)
 };
 
