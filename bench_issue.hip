@@ -28,6 +28,14 @@
 //   soft+m32 soft with one 32x32x64 MFMA after every 4 scores' worth of
 //            softmax instructions (16 per iteration)
 //   soft+m16 soft with one 16x16x128 MFMA after every 2 scores (32)
+//   tile     the whole vector and matrix-core mix of one wave-tile of the
+//            attention kernel as compiled: soft, 16 32x32x64 and 2 16x16x128
+//            products in the kernel's order (the previous tile's second PV
+//            chunk and the first score pair under the first quarter of the
+//            softmax, a score pair and the first PV chunk under the second,
+//            a score pair under each of the last two), plus 3 FMA, 3 exp,
+//            3 max3, 20 integer operations and 11 multiplies (the rescale of
+//            O~, which runs on about 16 % of tiles, averaged)
 //   idle     nothing (the wave exits at once)
 #include <hip/hip_runtime.h>
 
@@ -41,9 +49,9 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef int v4i __attribute__((ext_vector_type(4)));
 
-enum Kind { kIdle, kFma, kExp, kCvt, kMax3, kSoft, kMfma32, kMfma16, kSoftM32, kSoftM16, kNumKinds };
+enum Kind { kIdle, kFma, kExp, kCvt, kMax3, kSoft, kMfma32, kMfma16, kSoftM32, kSoftM16, kTile, kNumKinds };
 static const char* kNames[kNumKinds] = {"idle", "fma", "exp", "cvt", "max3", "soft", "mfma32", "mfma16",
-                                        "soft+m32", "soft+m16"};
+                                        "soft+m32", "soft+m16", "tile"};
 
 constexpr int kIters = 512;        // A iterations
 constexpr int kMaxBIters = 1 << 16;  // cap on B iterations (B stops when A is done)
@@ -87,15 +95,16 @@ constexpr int kMaxBIters = 1 << 16;  // cap on B iterations (B stops when A is d
     MAX4(y, mx)
 
 template <int K>
-constexpr bool uses_m32() { return K == kMfma32 || K == kSoftM32; }
+constexpr bool uses_m32() { return K == kMfma32 || K == kSoftM32 || K == kTile; }
 template <int K>
-constexpr bool uses_m16() { return K == kMfma16 || K == kSoftM16; }
+constexpr bool uses_m16() { return K == kMfma16 || K == kSoftM16 || K == kTile; }
 
 // One iteration of stream K.
 template <int K>
 __device__ __forceinline__ void iteration(float (&x)[8], float (&y)[8], float (&mx)[4], uint32_t (&w)[4],
-                                          v16f (&acc32)[4], v4f (&acc16)[8], const v4i& a4, const v4i& b4,
-                                          const int& sc, float c1, float c2, float one) {
+                                          float (&z)[4], uint32_t (&ii)[4], v16f (&acc32)[4], v4f (&acc16)[8],
+                                          const v4i& a4, const v4i& b4, const int& sc, float c1, float c2,
+                                          float one) {
     if constexpr (K == kFma) {
         FMA8(x); FMA8(y); FMA8(x); FMA8(y); FMA8(x); FMA8(y); FMA8(x); FMA8(y);
     } else if constexpr (K == kExp) {
@@ -135,6 +144,29 @@ __device__ __forceinline__ void iteration(float (&x)[8], float (&y)[8], float (&
             FMA8(x); M16(acc16[0]); EXP8(x); M16(acc16[1]); CVT4(x, w); M16(acc16[2]); MAX4(y, mx); M16(acc16[3]);
             FMA8(y); M16(acc16[4]); EXP8(y); M16(acc16[5]); CVT4(y, w); M16(acc16[6]); MAX4(x, mx); M16(acc16[7]);
         }
+    } else if constexpr (K == kTile) {
+        // first quarter: the previous tile's second PV chunk, the first score pair
+        FMA8(x); M32(acc32[0]); EXP8(x); M32(acc32[1]); CVT4(x, w); M32(acc32[2]); MAX4(y, mx); M32(acc32[3]);
+        FMA8(y); M16(acc16[0]); EXP8(y); M32(acc32[0]); CVT4(y, w); MAX4(x, mx); M32(acc32[1]);
+        // second quarter: a score pair, the first PV chunk
+        FMA8(x); M32(acc32[2]); EXP8(x); M32(acc32[3]); CVT4(x, w); M32(acc32[0]); MAX4(y, mx); M32(acc32[1]);
+        FMA8(y); M32(acc32[2]); EXP8(y); M32(acc32[3]); CVT4(y, w); M16(acc16[1]); MAX4(x, mx);
+        // third and fourth quarters: a score pair each
+        FMA8(x); EXP8(x); M32(acc32[0]); CVT4(x, w); MAX4(y, mx);
+        FMA8(y); EXP8(y); M32(acc32[1]); CVT4(y, w); MAX4(x, mx);
+        FMA8(x); EXP8(x); M32(acc32[2]); CVT4(x, w); MAX4(y, mx);
+        FMA8(y); EXP8(y); M32(acc32[3]); CVT4(y, w); MAX4(x, mx);
+        // the rest of the tile's vector work
+#pragma unroll
+        for (int i = 0; i < 3; i++) {
+            asm volatile("v_fma_f32 %0, %0, %1, %2" : "+v"(z[i]) : "v"(c1), "v"(c2));
+            asm volatile("v_exp_f32 %0, %0" : "+v"(z[i + 1]));
+            asm volatile("v_maximum3_f32 %0, %0, %1, %2" : "+v"(z[3 - i]) : "v"(x[i]), "v"(y[i]));
+        }
+#pragma unroll
+        for (int i = 0; i < 20; i++) asm volatile("v_add_u32 %0, %0, %1" : "+v"(ii[i & 3]) : "v"(w[i & 3]));
+#pragma unroll
+        for (int i = 0; i < 11; i++) asm volatile("v_mul_f32 %0, %0, %1" : "+v"(z[i & 3]) : "v"(one));
     }
 }
 
@@ -150,7 +182,8 @@ __global__ __launch_bounds__(1024, 1) void issue_kernel(long long* out) {
     const int n_a = KB < 0 ? nwaves : 4;
     if (threadIdx.x == 0) done_count = 0;
 
-    float x[8], y[8], mx[4] = {0.f, 0.f, 0.f, 0.f};
+    float x[8], y[8], mx[4] = {0.f, 0.f, 0.f, 0.f}, z[4] = {-0.5f, -0.25f, -0.125f, -1.f};
+    uint32_t ii[4] = {1, 2, 3, 4};
     uint32_t w[4] = {0, 0, 0, 0};
     for (int i = 0; i < 8; i++) {
         x[i] = 1e-3f * (float)(i + 1 + (threadIdx.x & 7));
@@ -176,14 +209,14 @@ __global__ __launch_bounds__(1024, 1) void issue_kernel(long long* out) {
     int iters = 0;
     if (is_a) {
         for (int it = 0; it < kIters; it++) {
-            iteration<KA>(x, y, mx, w, acc32, acc16, a4, b4, sc, c1, c2, one);
+            iteration<KA>(x, y, mx, w, z, ii, acc32, acc16, a4, b4, sc, c1, c2, one);
             iters++;
         }
     } else if constexpr (KB >= 0) {
         for (int it = 0; it < kMaxBIters; it++) {
             // stop once every A wave has finished
             if (__builtin_amdgcn_readfirstlane(*(volatile int*)&done_count) >= n_a) break;
-            iteration<KB>(x, y, mx, w, acc32, acc16, a4, b4, sc, c1, c2, one);
+            iteration<KB>(x, y, mx, w, z, ii, acc32, acc16, a4, b4, sc, c1, c2, one);
             iters++;
         }
     }
@@ -194,7 +227,7 @@ __global__ __launch_bounds__(1024, 1) void issue_kernel(long long* out) {
 
     float s = 0.f;
     for (int i = 0; i < 8; i++) s += x[i] + y[i];
-    for (int i = 0; i < 4; i++) s += __builtin_bit_cast(float, w[i]) + mx[i];
+    for (int i = 0; i < 4; i++) s += __builtin_bit_cast(float, w[i] ^ ii[i]) + mx[i] + z[i];
     if constexpr (uses_m32<KA>() || (KB >= 0 && uses_m32<KB>()))
         for (int k = 0; k < 4; k++) s += acc32[k][threadIdx.x & 15];
     if constexpr (uses_m16<KA>() || (KB >= 0 && uses_m16<KB>()))
@@ -268,7 +301,7 @@ int main() {
                            {kCvt, kfn<kCvt, -1>()},         {kMax3, kfn<kMax3, -1>()},
                            {kSoft, kfn<kSoft, -1>()},       {kMfma32, kfn<kMfma32, -1>()},
                            {kMfma16, kfn<kMfma16, -1>()},   {kSoftM32, kfn<kSoftM32, -1>()},
-                           {kSoftM16, kfn<kSoftM16, -1>()}};
+                           {kSoftM16, kfn<kSoftM16, -1>()},   {kTile, kfn<kTile, -1>()}};
     for (const Alone& a : alone)
         for (int slots : {1, 2, 3, 4}) {
             Result r = run(a.f, -1, slots, d, h);
