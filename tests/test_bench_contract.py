@@ -46,3 +46,22 @@ def test_traffic_record(path):
         current = hashlib.sha256(f.read()).hexdigest() == rec["kernel_source_sha256"]
     got = bench.measured_traffic(name, rec["mode"])
     assert got == (rec["hbm_bytes_per_launch"] if current else None)
+
+
+def test_stratified_oracle_sample_covers_every_head_and_the_edges():
+    """The bounded oracle sample of `bench.py --cpu-table`: every head gets
+    its share, the first and the ragged last query tile and the sequence's
+    end are in every head's rows, and each text row is in exactly one head."""
+    N, heads, text = 3001, 5, 40
+    rows = bench.stratified_rows(N, heads, 52, seed=3, text_tokens=text)
+    assert sorted(rows) == list(range(heads))
+    last = (N - 1) // 128 * 128
+    for h, r in rows.items():
+        assert r.size == 52 and r.dtype.kind == "i"
+        assert len(set(r.tolist())) == r.size and r.min() >= 0 and r.max() < N
+        assert {0, 1, 63, 127, last, last + 1, N - 2, N - 1} <= set(r.tolist())
+    text_rows = [x for r in rows.values() for x in r.tolist() if x >= N - text]
+    fixed = {N - 2, N - 1}  # in every head's rows anyway
+    assert sorted(set(text_rows) - fixed) == sorted(set(range(N - text, N)) - fixed)
+    # a sequence shorter than the sample takes every row
+    assert bench.stratified_rows(100, 2, 300, seed=1)[1].tolist() == list(range(100))
