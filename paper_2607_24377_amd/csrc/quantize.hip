@@ -27,6 +27,41 @@ __device__ __forceinline__ uint4 nt_load(const uint4* p) {
 // loaded before either is quantized; the 4 threads of a 32-element block are
 // adjacent lanes and exchange their maxima with two lane swaps.
 // ---------------------------------------------------------------------------
+// Cross-lane exchanges inside a row of 16 lanes with DPP moves (no LDS
+// traffic): the value of lane i ^ kM.  xor 1 and 2 are quad permutations;
+// xor 4 and 8 compose the half-row mirror (lane i ^ 7) with the quad
+// reversal (^ 3) or with the row mirror (^ 15).
+template <int kM>
+__device__ __forceinline__ int lane_xor(int v) {
+    constexpr int kQuadXor1 = 0xB1, kQuadXor2 = 0x4E, kQuadRev = 0x1B, kRowMirror = 0x140, kHalfMirror = 0x141;
+    if constexpr (kM == 1) {
+        return __builtin_amdgcn_mov_dpp(v, kQuadXor1, 0xF, 0xF, false);
+    } else if constexpr (kM == 2) {
+        return __builtin_amdgcn_mov_dpp(v, kQuadXor2, 0xF, 0xF, false);
+    } else if constexpr (kM == 4) {
+        const int h = __builtin_amdgcn_mov_dpp(v, kHalfMirror, 0xF, 0xF, false);
+        return __builtin_amdgcn_mov_dpp(h, kQuadRev, 0xF, 0xF, false);
+    } else {
+        static_assert(kM == 8, "xor within a row of 16 lanes");
+        const int h = __builtin_amdgcn_mov_dpp(v, kHalfMirror, 0xF, 0xF, false);
+        return __builtin_amdgcn_mov_dpp(h, kRowMirror, 0xF, 0xF, false);
+    }
+}
+template <int kM>
+__device__ __forceinline__ float lane_xor(float v) {
+    return __builtin_bit_cast(float, lane_xor<kM>(__builtin_bit_cast(int, v)));
+}
+
+// One cross-lane butterfly stage of the Walsh-Hadamard transform over the 16
+// lanes of a row: lane t gets a + b (lower partner) or a - b (upper), with a
+// the lower lane's value; fma with +-1 rounds exactly as the add or subtract.
+template <int kM>
+__device__ __forceinline__ void butterfly_lanes(float (&y)[8], int t) {
+    const float sgn = (t & kM) ? -1.f : 1.f;
+#pragma unroll
+    for (int e = 0; e < 8; e++) y[e] = __builtin_fmaf(sgn, y[e], lane_xor<kM>(y[e]));
+}
+
 // Quantizes the 16-byte chunk v (8 elements) of chunk index i.
 template <int kRule>
 __device__ __forceinline__ void quantize_chunk(uint4 v, int64_t i, bool valid, uint32_t* __restrict__ codes,
@@ -42,8 +77,8 @@ __device__ __forceinline__ void quantize_chunk(uint4 v, int64_t i, bool valid, u
     m = max(m, (v.z >> 16) & 0x7FFFu);
     m = max(m, v.w & 0x7FFFu);
     m = max(m, (v.w >> 16) & 0x7FFFu);
-    m = max(m, (uint32_t)__shfl_xor((int)m, 1));
-    m = max(m, (uint32_t)__shfl_xor((int)m, 2));
+    m = max(m, (uint32_t)lane_xor<1>((int)m));
+    m = max(m, (uint32_t)lane_xor<2>((int)m));
     // all-zero block: sigma = 1 (Algorithm 1); codes come out as signed zeros
     const uint32_t sbyte = (m == 0) ? 127u : (uint32_t)(block_exponent_bf16<kRule>(m, bq) + 127);
     const float sf = e8m0_as_f32(sbyte);
@@ -118,15 +153,10 @@ __global__ __launch_bounds__(256) void quantize_headdim_rot_kernel(const uint4* 
             y[e + h] = a - b;
         }
     }
-#pragma unroll
-    for (int m = 1; m < 16; m *= 2) {
-        const bool upper = (t & m) != 0;
-#pragma unroll
-        for (int e = 0; e < 8; e++) {
-            const float other = __shfl_xor(y[e], m);
-            y[e] = upper ? other - y[e] : y[e] + other;
-        }
-    }
+    butterfly_lanes<1>(y, t);
+    butterfly_lanes<2>(y, t);
+    butterfly_lanes<4>(y, t);
+    butterfly_lanes<8>(y, t);
     const float rs = 0.0883883476483184405f;  // fp32(1/sqrt(128))
 #pragma unroll
     for (int e = 0; e < 8; e++) y[e] = y[e] * rs;
@@ -135,8 +165,8 @@ __global__ __launch_bounds__(256) void quantize_headdim_rot_kernel(const uint4* 
     uint32_t m = 0;
 #pragma unroll
     for (int e = 0; e < 8; e++) m = max(m, __builtin_bit_cast(uint32_t, y[e]) & 0x7FFFFFFFu);
-    m = max(m, (uint32_t)__shfl_xor((int)m, 1));
-    m = max(m, (uint32_t)__shfl_xor((int)m, 2));
+    m = max(m, (uint32_t)lane_xor<1>((int)m));
+    m = max(m, (uint32_t)lane_xor<2>((int)m));
     const uint32_t sbyte = (m == 0) ? 127u : (uint32_t)(scale_exponent_f32<kRule>(m) + 127);
     const float sf = e8m0_as_f32(sbyte);
 
