@@ -52,9 +52,10 @@ __device__ __forceinline__ float lane_xor(float v) {
     return __builtin_bit_cast(float, lane_xor<kM>(__builtin_bit_cast(int, v)));
 }
 
-// One cross-lane butterfly stage of the Walsh-Hadamard transform over the 16
-// lanes of a row: lane t gets a + b (lower partner) or a - b (upper), with a
-// the lower lane's value; fma with +-1 rounds exactly as the add or subtract.
+// One cross-lane butterfly stage of the Walsh-Hadamard transform over the
+// lanes of a row (partners differ in bit kM of the lane's index t): lane t gets
+// a + b (lower partner) or a - b (upper), with a the lower lane's value; fma
+// with +-1 rounds exactly as the add or subtract.
 template <int kM>
 __device__ __forceinline__ void butterfly_lanes(float (&y)[8], int t) {
     const float sgn = (t & kM) ? -1.f : 1.f;
@@ -119,65 +120,84 @@ __global__ __launch_bounds__(256) void quantize_headdim_kernel(const uint4* __re
 // 2) before the block quantization above.  The product is the radix-2 fast
 // Walsh-Hadamard transform in fp32, stages h = 1, 2, 4, ..., 64, each mapping
 // (x[i], x[i+h]) (bit h of i clear) to (a + b, a - b), then one fp32 multiply
-// by fp32(1/sqrt(128)); the 16 threads of a row hold 8 consecutive elements
-// each, so stages 1-4 run in registers and stages 8-64 swap with the thread
-// whose row index differs in bit 0-3.  Every operation is a single correctly
+// by fp32(1/sqrt(128)); the 8 threads of a row hold 16 consecutive elements
+// each, so stages 1-8 run in registers and stages 16-64 exchange with the
+// thread whose index in the row differs in bit 0, 1 or 2 (DPP moves inside the
+// row of lanes).  Every operation is a single correctly
 // rounded fp32 add, subtract or multiply in a fixed order, so the result is
 // bit-identical to any other evaluation in that order.
 // ---------------------------------------------------------------------------
 template <int kRule>
 __global__ __launch_bounds__(256) void quantize_headdim_rot_kernel(const uint4* __restrict__ x,
-                                                                   uint32_t* __restrict__ codes,
+                                                                   uint2* __restrict__ codes,
                                                                    uint8_t* __restrict__ scales,
-                                                                   int64_t n_chunks) {
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    const bool valid = i < n_chunks;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (valid) v = nt_load(x + i);
-    const int t = threadIdx.x & 15;  // thread within the row: elements 8t..8t+7
+                                                                   int64_t n_threads) {
+    // 8 lanes per row of 128, 16 consecutive elements (two chunks) each
+    const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const bool valid = g < n_threads;
+    uint4 v0 = make_uint4(0, 0, 0, 0), v1 = v0;
+    if (valid) {
+        v0 = nt_load(x + 2 * g);
+        v1 = nt_load(x + 2 * g + 1);
+    }
+    const int t = threadIdx.x & 7;  // thread within the row: elements 16t..16t+15
 
-    float y[8];
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    float y[16];
+    const uint32_t w[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
 #pragma unroll
-    for (int e = 0; e < 4; e++) {
+    for (int e = 0; e < 8; e++) {
         y[2 * e] = __builtin_bit_cast(float, w[e] << 16);
         y[2 * e + 1] = __builtin_bit_cast(float, w[e] & 0xFFFF0000u);
     }
 #pragma unroll
-    for (int h = 1; h < 8; h *= 2) {
+    for (int h = 1; h < 16; h *= 2) {
 #pragma unroll
-        for (int e = 0; e < 8; e++) {
+        for (int e = 0; e < 16; e++) {
             if (e & h) continue;
             const float a = y[e], b = y[e + h];
             y[e] = a + b;
             y[e + h] = a - b;
         }
     }
-    butterfly_lanes<1>(y, t);
-    butterfly_lanes<2>(y, t);
-    butterfly_lanes<4>(y, t);
-    butterfly_lanes<8>(y, t);
+#pragma unroll
+    for (int half = 0; half < 2; half++) {
+        float (&yh)[8] = *reinterpret_cast<float(*)[8]>(&y[8 * half]);
+        butterfly_lanes<1>(yh, t);
+    }
+#pragma unroll
+    for (int half = 0; half < 2; half++) {
+        float (&yh)[8] = *reinterpret_cast<float(*)[8]>(&y[8 * half]);
+        butterfly_lanes<2>(yh, t);
+    }
+#pragma unroll
+    for (int half = 0; half < 2; half++) {
+        float (&yh)[8] = *reinterpret_cast<float(*)[8]>(&y[8 * half]);
+        butterfly_lanes<4>(yh, t);
+    }
     const float rs = 0.0883883476483184405f;  // fp32(1/sqrt(128))
 #pragma unroll
-    for (int e = 0; e < 8; e++) y[e] = y[e] * rs;
+    for (int e = 0; e < 16; e++) y[e] = y[e] * rs;
 
-    // block maximum of |y| on the fp32 bit patterns
+    // block maximum of |y| on the fp32 bit patterns: two lanes per block
     uint32_t m = 0;
 #pragma unroll
-    for (int e = 0; e < 8; e++) m = max(m, __builtin_bit_cast(uint32_t, y[e]) & 0x7FFFFFFFu);
+    for (int e = 0; e < 16; e++) m = max(m, __builtin_bit_cast(uint32_t, y[e]) & 0x7FFFFFFFu);
     m = max(m, (uint32_t)lane_xor<1>((int)m));
-    m = max(m, (uint32_t)lane_xor<2>((int)m));
     const uint32_t sbyte = (m == 0) ? 127u : (uint32_t)(scale_exponent_f32<kRule>(m) + 127);
     const float sf = e8m0_as_f32(sbyte);
 
-    uint32_t c = 0;
-    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[0], y[1], sf, 0);
-    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[2], y[3], sf, 1);
-    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[4], y[5], sf, 2);
-    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[6], y[7], sf, 3);
+    uint32_t c0 = 0, c1 = 0;
+    c0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c0, y[0], y[1], sf, 0);
+    c0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c0, y[2], y[3], sf, 1);
+    c0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c0, y[4], y[5], sf, 2);
+    c0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c0, y[6], y[7], sf, 3);
+    c1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c1, y[8], y[9], sf, 0);
+    c1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c1, y[10], y[11], sf, 1);
+    c1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c1, y[12], y[13], sf, 2);
+    c1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c1, y[14], y[15], sf, 3);
     if (valid) {
-        codes[i] = c;
-        if ((i & 3) == 0) scales[i >> 2] = (uint8_t)sbyte;
+        codes[g] = make_uint2(c0, c1);
+        if ((g & 1) == 0) scales[g >> 1] = (uint8_t)sbyte;
     }
 }
 
@@ -326,15 +346,15 @@ hipError_t launch_quantize_headdim(const void* x, uint8_t* codes, uint8_t* scale
 
 hipError_t launch_quantize_headdim_rotated(const void* x, uint8_t* codes, uint8_t* scales, int64_t rows,
                                            int rule, hipStream_t stream) {
-    const int64_t n_chunks = rows * 16;
-    if (n_chunks == 0) return hipSuccess;
-    const dim3 grid((unsigned)((n_chunks + 255) / 256));
+    const int64_t n_threads = rows * 8;
+    if (n_threads == 0) return hipSuccess;
+    const dim3 grid((unsigned)((n_threads + 255) / 256));
     if (rule == kRuleUos)
         quantize_headdim_rot_kernel<kRuleUos><<<grid, 256, 0, stream>>>(
-            (const uint4*)x, (uint32_t*)codes, scales, n_chunks);
+            (const uint4*)x, (uint2*)codes, scales, n_threads);
     else
         quantize_headdim_rot_kernel<kRuleOcp><<<grid, 256, 0, stream>>>(
-            (const uint4*)x, (uint32_t*)codes, scales, n_chunks);
+            (const uint4*)x, (uint2*)codes, scales, n_threads);
     return hipGetLastError();
 }
 
